@@ -1,0 +1,914 @@
+// C ABI of the layer-shard library: argument validation, the exact memory
+// estimate, the arena / activation-stash allocator, kernel timing, and the
+// orchestration of the forward, backward and LM-head kernel sequences.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "../../include/l4d.h"
+#include "kernels.h"
+
+using namespace l4d;
+
+// ============================================================== errors
+
+static thread_local std::string g_err;
+
+static int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+extern "C" const char* l4d_last_error(void) { return g_err.c_str(); }
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess) return fail(L4D_EDEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+// ============================================================== kernel timing
+
+namespace {
+struct Pending {
+  const char* name;
+  hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<Pending> g_pending;
+std::vector<hipEvent_t> g_event_pool;
+std::map<std::string, std::pair<int64_t, double>> g_totals;
+
+hipEvent_t take_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+int drain_pending() {
+  for (auto& p : g_pending) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(p.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.a, p.b);
+    if (e != hipSuccess) return fail(L4D_EDEVICE, "profile events: %s", hipGetErrorString(e));
+    auto& t = g_totals[p.name];
+    t.first += 1;
+    t.second += ms;
+    g_event_pool.push_back(p.a);
+    g_event_pool.push_back(p.b);
+  }
+  g_pending.clear();
+  return L4D_OK;
+}
+
+// Launch `fn` (returning hipError_t) bracketed by events when timing is on.
+template <class F>
+int launch(const char* name, hipStream_t s, F&& fn) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (g_prof_on) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    a = take_event();
+    b = take_event();
+    if (a) (void)hipEventRecord(a, s);
+  }
+  hipError_t e = fn();
+  if (e != hipSuccess) return fail(L4D_EDEVICE, "launch of %s failed: %s", name, hipGetErrorString(e));
+  if (a && b) {
+    (void)hipEventRecord(b, s);
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_pending.push_back({name, a, b});
+  }
+  return L4D_OK;
+}
+}  // namespace
+
+extern "C" int l4d_profile_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_on = on != 0;
+  return L4D_OK;
+}
+
+extern "C" int l4d_profile_reset(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  int rc = drain_pending();
+  g_totals.clear();
+  return rc;
+}
+
+extern "C" int l4d_profile_read(const char* name, int64_t* launches, double* total_ms) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  int rc = drain_pending();
+  if (rc) return rc;
+  int64_t n = 0;
+  double ms = 0;
+  for (auto& kv : g_totals)
+    if (!name || kv.first == name) {
+      n += kv.second.first;
+      ms += kv.second.second;
+    }
+  if (launches) *launches = n;
+  if (total_ms) *total_ms = ms;
+  return L4D_OK;
+}
+
+extern "C" int l4d_profile_dump(char* buf, uint64_t buf_len, uint64_t* needed) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  int rc = drain_pending();
+  if (rc) return rc;
+  std::string out;
+  char line[256];
+  for (auto& kv : g_totals) {
+    snprintf(line, sizeof line, "%s %lld %.6f\n", kv.first.c_str(), (long long)kv.second.first, kv.second.second);
+    out += line;
+  }
+  if (needed) *needed = out.size() + 1;
+  if (buf && buf_len) {
+    size_t n = std::min<size_t>(out.size(), buf_len - 1);
+    memcpy(buf, out.data(), n);
+    buf[n] = 0;
+  }
+  return L4D_OK;
+}
+
+// ============================================================== memory estimate
+
+namespace {
+typedef __int128 i128;
+
+struct Rat {  // num / den, den > 0
+  i128 num, den;
+};
+
+uint64_t ceil_u64(Rat r, bool& inexact) {
+  i128 q = r.num / r.den, rem = r.num % r.den;
+  if (rem != 0) {
+    inexact = true;
+    q += 1;
+  }
+  return (uint64_t)q;
+}
+
+int check_model(const l4d_model* m, const l4d_parallel* p) {
+  if (!m || !p) return fail(L4D_EINVAL, "model and parallel layout are required");
+  if (m->hidden <= 0 || m->n_heads <= 0 || m->n_kv_heads <= 0 || m->ffn <= 0 || m->n_layers <= 0 ||
+      m->vocab <= 0)
+    return fail(L4D_EINVAL, "model sizes must be positive");
+  if (p->seq <= 0 || p->micro_batch <= 0 || p->tp <= 0 || p->cp <= 0 || p->pp <= 0 || p->dp <= 0)
+    return fail(L4D_EINVAL, "sequence, micro-batch and parallel sizes must be positive");
+  if (m->hidden % m->n_heads) return fail(L4D_EINVAL, "hidden %% n_heads != 0");
+  if (m->n_heads % m->n_kv_heads) return fail(L4D_EINVAL, "n_heads %% n_kv_heads != 0");
+  if (m->n_heads % p->tp || m->n_kv_heads % p->tp) return fail(L4D_EINVAL, "heads not divisible by tp");
+  if (m->ffn % p->tp) return fail(L4D_EINVAL, "ffn %% tp != 0");
+  if (m->vocab % p->tp) return fail(L4D_EINVAL, "vocab %% tp != 0");
+  if (p->seq % p->cp) return fail(L4D_EINVAL, "seq %% cp != 0");
+  if (m->n_layers % p->pp) return fail(L4D_EINVAL, "n_layers %% pp != 0");
+  if (p->tp_rank < 0 || p->tp_rank >= p->tp || p->cp_rank < 0 || p->cp_rank >= p->cp)
+    return fail(L4D_EINVAL, "rank out of range");
+  return L4D_OK;
+}
+}  // namespace
+
+extern "C" int mem_estimate(const l4d_model* m, const l4d_parallel* p, l4d_mem* out) {
+  int rc = check_model(m, p);
+  if (rc) return rc;
+  if (!out) return fail(L4D_EINVAL, "out is NULL");
+  const i128 h = m->hidden, a = m->n_heads, k = m->n_kv_heads, f = m->ffn, L = m->n_layers, v = m->vocab;
+  const i128 s = p->seq, b = p->micro_batch, t = p->tp, c = p->cp, pp = p->pp, d = p->dp;
+  // ell * (a t) = 2h^2(a+k) + 3 h f a + 2 h a t   (Eqs. 1, 2 divided by t, plus the two norms)
+  const i128 E = 2 * h * h * (a + k) + 3 * h * f * a + 2 * h * a * t;
+  Rat psi;
+  if (p->pp == 1) psi = {2 * h * v * a + h * a * t + L * E, a * t};   // embedding + head + final norm
+  else psi = {h * v * a * pp + L * E, a * t * pp};                   // first stage (Eq. 7)
+  bool inexact = false;
+  out->params_per_gpu = ceil_u64(psi, inexact);
+  out->weight_bytes = ceil_u64({2 * psi.num, psi.den}, inexact);
+  out->grad_bytes = ceil_u64({4 * psi.num, psi.den}, inexact);
+  out->optim_bytes = ceil_u64({12 * psi.num, psi.den * d * c}, inexact);
+  // per layer: s b (12 a h + 4 k h + 8 f a) / (t c a)     (Eq. 12 / (tc))
+  const i128 lay = 12 * a * h + 4 * k * h + 8 * f * a;
+  out->act_bytes_per_layer = ceil_u64({s * b * lay, t * c * a}, inexact);
+  // Eq. 17: s b [L lay + 8 p a h + [p=1] 4 a (h + v)] / (t c a)
+  i128 act = L * lay + 8 * pp * a * h;
+  if (p->pp == 1) act += 4 * a * (h + v);
+  out->act_bytes = ceil_u64({s * b * act, t * c * a}, inexact);
+  out->total_bytes = out->weight_bytes + out->grad_bytes + out->optim_bytes + out->act_bytes;
+  out->inexact = inexact ? 1u : 0u;
+  return L4D_OK;
+}
+
+// ============================================================== arena
+
+struct l4d_arena {
+  uintptr_t base;
+  uint64_t cap;
+  std::map<uint64_t, uint64_t> free_;  // offset -> size
+  uint64_t in_use = 0, peak = 0;
+  std::set<const l4d_stash*> live;
+};
+
+namespace {
+constexpr uint64_t kAlign = 256;
+uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool arena_alloc(l4d_arena* A, uint64_t size, uint64_t* off) {
+  size = align_up(std::max<uint64_t>(size, 1));
+  for (auto it = A->free_.begin(); it != A->free_.end(); ++it) {
+    if (it->second >= size) {
+      *off = it->first;
+      uint64_t rest = it->second - size, roff = it->first + size;
+      A->free_.erase(it);
+      if (rest) A->free_[roff] = rest;
+      A->in_use += size;
+      A->peak = std::max(A->peak, A->in_use);
+      return true;
+    }
+  }
+  return false;
+}
+
+void arena_free(l4d_arena* A, uint64_t off, uint64_t size) {
+  size = align_up(std::max<uint64_t>(size, 1));
+  A->in_use -= size;
+  auto it = A->free_.emplace(off, size).first;
+  auto nx = std::next(it);
+  if (nx != A->free_.end() && it->first + it->second == nx->first) {
+    it->second += nx->second;
+    A->free_.erase(nx);
+  }
+  if (it != A->free_.begin()) {
+    auto pv = std::prev(it);
+    if (pv->first + pv->second == it->first) {
+      pv->second += it->second;
+      A->free_.erase(it);
+    }
+  }
+}
+
+// A transient workspace: a list of sub-buffers carved from one arena block.
+struct Workspace {
+  l4d_arena* A = nullptr;
+  uint64_t off = 0, size = 0;
+  bool held = false;
+  ~Workspace() {
+    if (held) arena_free(A, off, size);
+  }
+};
+
+struct Carver {  // bump-allocates aligned pieces of a byte range
+  uint64_t used = 0;
+  uint64_t take(uint64_t bytes) {
+    uint64_t o = used;
+    used += align_up(bytes);
+    return o;
+  }
+};
+}  // namespace
+
+extern "C" int l4d_arena_create(void* dev_base, uint64_t capacity, l4d_arena** out) {
+  if (!out) return fail(L4D_EINVAL, "out is NULL");
+  if (!dev_base && capacity) return fail(L4D_EINVAL, "dev_base is NULL");
+  if (reinterpret_cast<uintptr_t>(dev_base) % kAlign) return fail(L4D_EINVAL, "dev_base must be 256-byte aligned");
+  auto* A = new l4d_arena();
+  A->base = reinterpret_cast<uintptr_t>(dev_base);
+  A->cap = capacity / kAlign * kAlign;
+  if (A->cap) A->free_[0] = A->cap;
+  *out = A;
+  return L4D_OK;
+}
+
+extern "C" int l4d_arena_destroy(l4d_arena* A) {
+  if (!A) return L4D_OK;
+  if (!A->live.empty()) return fail(L4D_EINVAL, "arena still holds %zu live stash(es)", A->live.size());
+  delete A;
+  return L4D_OK;
+}
+
+extern "C" int l4d_arena_stats(const l4d_arena* A, uint64_t* in_use, uint64_t* peak, uint64_t* capacity) {
+  if (!A) return fail(L4D_EINVAL, "arena is NULL");
+  if (in_use) *in_use = A->in_use;
+  if (peak) *peak = A->peak;
+  if (capacity) *capacity = A->cap;
+  return L4D_OK;
+}
+
+// ============================================================== shard geometry
+
+namespace {
+struct Shard {
+  int64_t h, a, k, f, s, b, t, c, tr, cr;
+  int64_t d, a_t, k_t, f_t, s_c, s_sp;
+  float eps, base;
+  ChunkMap qmap;
+  int n_remote_runs;
+  int64_t rem_chunk_start[4], rem_chunk_count[4];  // runs of consecutive remote chunks (chunk ids)
+  int64_t chunk_len;
+};
+
+int make_shard(const l4d_model* m, const l4d_parallel* p, Shard* S) {
+  int rc = check_model(m, p);
+  if (rc) return rc;
+  Shard& x = *S;
+  x.h = m->hidden; x.a = m->n_heads; x.k = m->n_kv_heads; x.f = m->ffn;
+  x.s = p->seq; x.b = p->micro_batch; x.t = p->tp; x.c = p->cp; x.tr = p->tp_rank; x.cr = p->cp_rank;
+  x.eps = m->rms_eps; x.base = m->rope_base;
+  x.d = x.h / x.a; x.a_t = x.a / x.t; x.k_t = x.k / x.t; x.f_t = x.f / x.t;
+  x.s_c = x.s / x.c;
+  if (x.s_c % x.t) return fail(L4D_EINVAL, "local sequence %lld not divisible by tp", (long long)x.s_c);
+  x.s_sp = x.s_c / x.t;
+  if (x.d != 64 && x.d != 128) return fail(L4D_EINVAL, "head dim %lld unsupported (64 or 128)", (long long)x.d);
+  if (x.h % 8 || x.f_t % 8) return fail(L4D_EINVAL, "hidden and ffn/tp must be multiples of 8");
+  if (x.h > 8192) return fail(L4D_EINVAL, "hidden > 8192 unsupported");
+  if (x.c > 1 && x.s % (2 * x.c)) return fail(L4D_EINVAL, "seq %% (2 cp) != 0");
+  if (x.b * x.s_c > (int64_t)1 << 30 || x.h * x.s > (int64_t)1 << 40)
+    return fail(L4D_EINVAL, "problem too large");
+  // CP layout: 2c chunks, rank r owns r and 2c-1-r (Sec. 2.1 / 3.2.3 load-balanced reading)
+  if (x.c == 1) {
+    x.chunk_len = x.s;
+    x.qmap = ChunkMap{1, (int32_t)x.s, {0, 0}};
+    x.n_remote_runs = 0;
+  } else {
+    x.chunk_len = x.s / (2 * x.c);
+    x.qmap = ChunkMap{2, (int32_t)x.chunk_len, {(int32_t)x.cr, (int32_t)(2 * x.c - 1 - x.cr)}};
+    x.n_remote_runs = 0;
+    int64_t i = 0;
+    while (i < 2 * x.c) {
+      if (i == x.cr || i == 2 * x.c - 1 - x.cr) { ++i; continue; }
+      int64_t j = i;
+      while (j + 1 < 2 * x.c && j + 1 != x.cr && j + 1 != 2 * x.c - 1 - x.cr) ++j;
+      x.rem_chunk_start[x.n_remote_runs] = i;
+      x.rem_chunk_count[x.n_remote_runs] = j - i + 1;
+      ++x.n_remote_runs;
+      i = j + 1;
+    }
+  }
+  return L4D_OK;
+}
+
+int64_t qkv_cols(const Shard& x) { return (x.a_t + 2 * x.k_t) * x.d; }
+}  // namespace
+
+// ============================================================== stash
+
+struct l4d_stash {
+  l4d_arena* arena;
+  uint64_t block_off, block_size;
+  uint64_t off[L4D_STASH_COUNT], bytes[L4D_STASH_COUNT];
+  uint64_t formula, aux, padding;
+  Shard shape;
+};
+
+namespace {
+void stash_sizes(const Shard& x, uint64_t* bytes) {
+  const uint64_t sp = x.b * x.s_sp * x.h * 2, tok = x.b * x.s_c;
+  bytes[L4D_STASH_X] = bytes[L4D_STASH_XN1] = bytes[L4D_STASH_H1] = bytes[L4D_STASH_XN2] = sp;
+  bytes[L4D_STASH_Q] = bytes[L4D_STASH_CTX] = tok * x.a_t * x.d * 2;
+  bytes[L4D_STASH_K] = bytes[L4D_STASH_V] = tok * x.k_t * x.d * 2;
+  bytes[L4D_STASH_GATE] = bytes[L4D_STASH_UP] = bytes[L4D_STASH_ACT] = bytes[L4D_STASH_PROD] = tok * x.f_t * 2;
+  bytes[L4D_STASH_LSE] = x.b * x.a_t * x.s_c * 4;
+}
+
+int stash_reserve(l4d_arena* A, const Shard& x, l4d_stash** out) {
+  auto* st = new l4d_stash();
+  st->arena = A;
+  st->shape = x;
+  stash_sizes(x, st->bytes);
+  uint64_t total = 0, raw = 0;
+  for (int i = 0; i < L4D_STASH_COUNT; ++i) {
+    st->off[i] = total;
+    total += align_up(st->bytes[i]);
+    if (i != L4D_STASH_LSE) raw += st->bytes[i];
+  }
+  st->formula = raw;
+  st->aux = st->bytes[L4D_STASH_LSE];
+  st->padding = total - raw - st->aux;
+  if (!arena_alloc(A, total, &st->block_off)) {
+    delete st;
+    return fail(L4D_ENOMEM, "stash needs %llu bytes; arena has %llu of %llu in use", (unsigned long long)total,
+                (unsigned long long)A->in_use, (unsigned long long)A->cap);
+  }
+  st->block_size = total;
+  A->live.insert(st);
+  *out = st;
+  return L4D_OK;
+}
+
+template <class T = uint16_t>
+T* sptr(const l4d_stash* st, int which) {
+  return reinterpret_cast<T*>(st->arena->base + st->block_off + st->off[which]);
+}
+}  // namespace
+
+extern "C" int l4d_stash_reserve(l4d_arena* A, const l4d_model* m, const l4d_parallel* p, l4d_stash** out) {
+  if (!A || !out) return fail(L4D_EINVAL, "arena and out are required");
+  Shard x;
+  int rc = make_shard(m, p, &x);
+  if (rc) return rc;
+  return stash_reserve(A, x, out);
+}
+
+extern "C" int l4d_stash_bytes(const l4d_stash* st, uint64_t* formula, uint64_t* aux, uint64_t* padding) {
+  if (!st) return fail(L4D_EINVAL, "stash is NULL");
+  if (formula) *formula = st->formula;
+  if (aux) *aux = st->aux;
+  if (padding) *padding = st->padding;
+  return L4D_OK;
+}
+
+extern "C" int l4d_stash_tensor(const l4d_stash* st, int which, void** ptr, uint64_t* bytes) {
+  if (!st) return fail(L4D_EINVAL, "stash is NULL");
+  if (which < 0 || which >= L4D_STASH_COUNT) return fail(L4D_EINVAL, "no stash tensor %d", which);
+  if (ptr) *ptr = sptr<void>(st, which);
+  if (bytes) *bytes = st->bytes[which];
+  return L4D_OK;
+}
+
+extern "C" int l4d_stash_release(l4d_arena* A, l4d_stash* st) {
+  if (!A || !st) return fail(L4D_EINVAL, "arena and stash are required");
+  if (st->arena != A || !A->live.count(st)) return fail(L4D_EINVAL, "stash does not belong to this arena");
+  arena_free(A, st->block_off, st->block_size);
+  A->live.erase(st);
+  delete st;
+  return L4D_OK;
+}
+
+// ============================================================== workspace plans
+
+namespace {
+struct FwdWs {
+  uint64_t rope, o_send, ffn_send, total;
+};
+struct BwdWs {
+  uint64_t rope, dgu, dxn2, dh1, dctx, delta, dqkv, dxn1, partial, dxn2_send, dxn1_send, total;
+};
+
+FwdWs plan_fwd(const Shard& x, const l4d_peer_outputs* sends) {
+  Carver cv;
+  FwdWs w;
+  const uint64_t peer_rows = x.b * (x.t - 1) * x.s_sp * x.h * 2;
+  w.rope = cv.take(x.s_c * (x.d / 2) * 8);
+  w.o_send = (x.t > 1 && !(sends && sends->o_partial)) ? cv.take(peer_rows) : 0;
+  w.ffn_send = (x.t > 1 && !(sends && sends->ffn_partial)) ? cv.take(peer_rows) : 0;
+  w.total = cv.used;
+  return w;
+}
+
+BwdWs plan_bwd(const Shard& x, const l4d_peer_outputs* sends) {
+  Carver cv;
+  BwdWs w;
+  const uint64_t tok = x.b * x.s_c, sp = x.b * x.s_sp * x.h * 2;
+  const uint64_t peer_rows = x.b * (x.t - 1) * x.s_sp * x.h * 2;
+  w.rope = cv.take(x.s_c * (x.d / 2) * 8);
+  w.dgu = cv.take(tok * 2 * x.f_t * 2);
+  w.dxn2 = cv.take(sp);
+  w.dh1 = cv.take(sp);
+  w.dctx = cv.take(tok * x.a_t * x.d * 2);
+  w.delta = cv.take(x.b * x.a_t * x.s_c * 4);
+  w.dqkv = cv.take(tok * qkv_cols(x) * 2);
+  w.dxn1 = cv.take(sp);
+  w.partial = cv.take((uint64_t)rmsnorm_bwd_partials(x.b * x.s_sp) * x.h * 4);
+  w.dxn2_send = (x.t > 1 && !(sends && sends->dxn2_partial)) ? cv.take(peer_rows) : 0;
+  w.dxn1_send = (x.t > 1 && !(sends && sends->dxn1_partial)) ? cv.take(peer_rows) : 0;
+  w.total = cv.used;
+  return w;
+}
+
+int take_ws(l4d_arena* A, uint64_t bytes, Workspace& ws) {
+  ws.A = A;
+  ws.size = bytes;
+  if (!arena_alloc(A, bytes, &ws.off))
+    return fail(L4D_ENOMEM, "workspace needs %llu bytes; arena has %llu of %llu in use", (unsigned long long)bytes,
+                (unsigned long long)A->in_use, (unsigned long long)A->cap);
+  ws.held = true;
+  return L4D_OK;
+}
+}  // namespace
+
+extern "C" int l4d_layer_workspace_bytes(const l4d_model* m, const l4d_parallel* p, uint64_t* fwd, uint64_t* bwd) {
+  Shard x;
+  int rc = make_shard(m, p, &x);
+  if (rc) return rc;
+  if (fwd) *fwd = align_up(plan_fwd(x, nullptr).total);
+  if (bwd) *bwd = align_up(plan_bwd(x, nullptr).total);
+  return L4D_OK;
+}
+
+extern "C" int l4d_lm_head_workspace_bytes(int64_t n, int64_t h, int64_t v_t, uint64_t* bytes) {
+  if (n < 0 || h <= 0 || v_t <= 0) return fail(L4D_EINVAL, "bad LM-head sizes");
+  if (bytes) *bytes = align_up((uint64_t)n * v_t * 2);
+  return L4D_OK;
+}
+
+// ============================================================== layer helpers
+
+namespace {
+inline RowSrc gathered(const void* own, const void* peer, const Shard& x) {
+  if (x.t == 1) return RowSrc::plain(own, x.h);
+  return RowSrc{static_cast<const uint16_t*>(own), static_cast<const uint16_t*>(peer), x.h, (int32_t)x.s_c,
+                (int32_t)x.s_sp, (int32_t)x.tr, (int32_t)x.t};
+}
+
+inline Operand op(RowSrc src, int64_t rows) { return Operand{src, (int32_t)rows, 0, 0}; }
+
+inline EpiParams epi_residual(const Shard& x, uint16_t* own_out, const void* resid, const void* receipt,
+                              void* send) {
+  EpiParams e{};
+  e.kind = EpiKind::ResidualSP;
+  e.ldc = x.h;
+  e.own_out = own_out;
+  e.resid = static_cast<const uint16_t*>(resid);
+  e.receipt = static_cast<const uint16_t*>(receipt);
+  e.send = static_cast<uint16_t*>(send);
+  e.s_c = (int32_t)x.s_c;
+  e.s_sp = (int32_t)x.s_sp;
+  e.r = (int32_t)x.tr;
+  e.t = (int32_t)x.t;
+  return e;
+}
+
+inline EpiParams epi_acc(float* c, int64_t ldc) {
+  EpiParams e{};
+  e.kind = EpiKind::AccF32;
+  e.c = c;
+  e.ldc = ldc;
+  return e;
+}
+
+inline EpiParams epi_store(void* c, int64_t ldc) {
+  EpiParams e{};
+  e.kind = EpiKind::StoreBF16;
+  e.c = c;
+  e.ldc = ldc;
+  return e;
+}
+
+int run_gemm(const char* name, hipStream_t s, int64_t M, int64_t N, int64_t K, Operand A, Layout la, Operand B,
+             Layout lb, EpiParams e) {
+  GemmParams p{};
+  p.M = (int32_t)M;
+  p.N = (int32_t)N;
+  p.K = (int32_t)K;
+  p.A = A;
+  p.B = B;
+  p.epi = e;
+  return launch(name, s, [&] { return gemm(p, la, lb, s); });
+}
+
+// Key runs of the attention: local chunks (stash K/V) then remote runs.
+void key_segments(const Shard& x, AttnParams& ap, const uint16_t* K, const uint16_t* V, const uint16_t* rK,
+                  const uint16_t* rV, uint16_t* dqkv, uint16_t* d_rk, uint16_t* d_rv, const uint16_t* cp_dk,
+                  const uint16_t* cp_dv) {
+  const int64_t kvw = x.k_t * x.d, qc = qkv_cols(x);
+  ap.n_seg = 0;
+  const int n_local = x.c == 1 ? 1 : 2;
+  const int64_t run = x.c == 1 ? x.s : x.chunk_len;
+  for (int i = 0; i < n_local; ++i) {
+    KvSeg& g = ap.seg[ap.n_seg++];
+    g = KvSeg{};
+    const int64_t row0 = i * run;
+    g.k = K + row0 * kvw;
+    g.v = V + row0 * kvw;
+    g.ld = kvw;
+    g.bstride = x.s_c * kvw;
+    if (dqkv) {
+      g.dk = dqkv + row0 * qc + x.a_t * x.d;
+      g.dv = dqkv + row0 * qc + (x.a_t + x.k_t) * x.d;
+      g.d_ld = qc;
+      g.d_bstride = x.s_c * qc;
+    }
+    if (cp_dk) {
+      g.rk = cp_dk + row0 * kvw;
+      g.rv = cp_dv + row0 * kvw;
+    }
+    g.n = (int32_t)run;
+    g.pos0 = (int32_t)(x.qmap.chunk_id[i] * x.qmap.chunk_len);
+    g.rope = 1;
+    g.rope_row0 = (int32_t)row0;
+  }
+  int64_t rrow = 0;
+  const int64_t rem_tokens = x.s - x.s_c;
+  for (int r = 0; r < x.n_remote_runs; ++r) {
+    KvSeg& g = ap.seg[ap.n_seg++];
+    g = KvSeg{};
+    const int64_t n = x.rem_chunk_count[r] * x.chunk_len;
+    g.k = rK + rrow * kvw;
+    g.v = rV + rrow * kvw;
+    g.ld = kvw;
+    g.bstride = rem_tokens * kvw;
+    if (d_rk) {
+      g.dk = d_rk + rrow * kvw;
+      g.dv = d_rv + rrow * kvw;
+      g.d_ld = kvw;
+      g.d_bstride = rem_tokens * kvw;
+    }
+    g.n = (int32_t)n;
+    g.pos0 = (int32_t)(x.rem_chunk_start[r] * x.chunk_len);
+    g.rope = 0;
+    rrow += n;
+  }
+}
+
+AttnParams attn_params(const Shard& x) {
+  AttnParams ap{};
+  ap.b = (int32_t)x.b;
+  ap.a_t = (int32_t)x.a_t;
+  ap.k_t = (int32_t)x.k_t;
+  ap.d_h = (int32_t)x.d;
+  ap.n_q = (int32_t)x.s_c;
+  ap.q_ld = x.a_t * x.d;
+  ap.q_bstride = x.s_c * x.a_t * x.d;
+  ap.qmap = x.qmap;
+  ap.scale = 1.0f / std::sqrt((float)x.d);
+  return ap;
+}
+
+int check_peers(const Shard& x, const l4d_peer_inputs* pi, bool bwd) {
+  if (x.c > 1 && (!pi || !pi->remote_k || !pi->remote_v))
+    return fail(L4D_EINVAL, "cp > 1 needs remote_k and remote_v");
+  if (x.t > 1) {
+    if (!pi || !pi->sp_peer_xn1 || !pi->sp_peer_xn2)
+      return fail(L4D_EINVAL, "tp > 1 needs sp_peer_xn1 and sp_peer_xn2");
+    if (bwd && (!pi->sp_peer_dy || !pi->sp_peer_dh1))
+      return fail(L4D_EINVAL, "tp > 1 backward needs sp_peer_dy and sp_peer_dh1");
+  }
+  if (x.c > 1 && pi && ((pi->cp_peer_dk == nullptr) != (pi->cp_peer_dv == nullptr)))
+    return fail(L4D_EINVAL, "cp_peer_dk and cp_peer_dv go together");
+  return L4D_OK;
+}
+}  // namespace
+
+// ============================================================== layer forward
+
+extern "C" int llama_layer_fwd(const l4d_model* m, const l4d_parallel* p, const l4d_layer_weights* w,
+                               const void* x_in, const l4d_peer_inputs* peers, const l4d_peer_outputs* sends,
+                               void* y, l4d_arena* A, l4d_stash** stash_out, void* stream_ptr) {
+  Shard x;
+  int rc = make_shard(m, p, &x);
+  if (rc) return rc;
+  if (!w || !w->norm1 || !w->qkv || !w->o || !w->norm2 || !w->gate_up || !w->down)
+    return fail(L4D_EINVAL, "all six weights are required");
+  if (!x_in || !y || !A || !stash_out) return fail(L4D_EINVAL, "x, y, arena and stash_out are required");
+  if ((rc = check_peers(x, peers, false))) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream_ptr);
+
+  const FwdWs plan = plan_fwd(x, sends);
+  l4d_stash* st = nullptr;
+  if ((rc = stash_reserve(A, x, &st))) return rc;
+  Workspace ws;
+  if ((rc = take_ws(A, plan.total, ws))) {
+    l4d_stash_release(A, st);
+    return rc;
+  }
+  uint8_t* wsb = reinterpret_cast<uint8_t*>(A->base + ws.off);
+  float2* rope = reinterpret_cast<float2*>(wsb + plan.rope);
+  const l4d_peer_inputs none{};
+  const l4d_peer_inputs& pi = peers ? *peers : none;
+  void* o_send = (sends && sends->o_partial) ? sends->o_partial : (void*)(wsb + plan.o_send);
+  void* ffn_send = (sends && sends->ffn_partial) ? sends->ffn_partial : (void*)(wsb + plan.ffn_send);
+  const int64_t tok = x.b * x.s_c, nq = x.a_t * x.d, nk = x.k_t * x.d;
+
+  auto body = [&]() -> int {
+    int r;
+    if ((r = launch("rope_table", s, [&] { return rope_table(rope, x.qmap, (int32_t)x.s_c, (int32_t)x.d, x.base, s); })))
+      return r;
+    // stash x (norm-1 input) and norm-1
+    HIP_TRY(hipMemcpyAsync(sptr(st, L4D_STASH_X), x_in, st->bytes[L4D_STASH_X], hipMemcpyDeviceToDevice, s));
+    if ((r = launch("rmsnorm_fwd", s, [&] {
+           return rmsnorm_fwd(static_cast<const uint16_t*>(x_in), static_cast<const uint16_t*>(w->norm1),
+                              sptr(st, L4D_STASH_XN1), x.b * x.s_sp, (int32_t)x.h, x.eps, s);
+         })))
+      return r;
+    // [Q|K|V] = xn1_full W_qkv^T, RoPE on Q, K
+    EpiParams eq{};
+    eq.kind = EpiKind::QkvRope;
+    eq.q = sptr(st, L4D_STASH_Q);
+    eq.k = sptr(st, L4D_STASH_K);
+    eq.v = sptr(st, L4D_STASH_V);
+    eq.nq = (int32_t)nq;
+    eq.nk = (int32_t)nk;
+    eq.rope = rope;
+    eq.d_h = (int32_t)x.d;
+    eq.s_c = (int32_t)x.s_c;
+    if ((r = run_gemm("gemm_qkv", s, tok, qkv_cols(x), x.h, op(gathered(sptr(st, L4D_STASH_XN1), pi.sp_peer_xn1, x), tok),
+                      Layout::KC, op(RowSrc::plain(w->qkv, x.h), qkv_cols(x)), Layout::KC, eq)))
+      return r;
+    // attention
+    AttnParams ap = attn_params(x);
+    ap.q = sptr(st, L4D_STASH_Q);
+    ap.o = sptr(st, L4D_STASH_CTX);
+    ap.lse = sptr<float>(st, L4D_STASH_LSE);
+    key_segments(x, ap, sptr(st, L4D_STASH_K), sptr(st, L4D_STASH_V), static_cast<const uint16_t*>(pi.remote_k),
+                 static_cast<const uint16_t*>(pi.remote_v), nullptr, nullptr, nullptr, nullptr, nullptr);
+    if ((r = launch("attn_fwd", s, [&] { return attn_fwd(ap, s); }))) return r;
+    // h1 = x + ctx W_o^T (own rows; peers' rows are sent)
+    if ((r = run_gemm("gemm_o", s, tok, x.h, nq, op(RowSrc::plain(sptr(st, L4D_STASH_CTX), nq), tok), Layout::KC,
+                      op(RowSrc::plain(w->o, nq), x.h), Layout::KC,
+                      epi_residual(x, sptr(st, L4D_STASH_H1), x_in, pi.sp_peer_o, o_send))))
+      return r;
+    if ((r = launch("rmsnorm_fwd", s, [&] {
+           return rmsnorm_fwd(sptr(st, L4D_STASH_H1), static_cast<const uint16_t*>(w->norm2), sptr(st, L4D_STASH_XN2),
+                              x.b * x.s_sp, (int32_t)x.h, x.eps, s);
+         })))
+      return r;
+    // [G|U] = xn2_full W_gu^T with the SwiGLU epilogue
+    EpiParams eg{};
+    eg.kind = EpiKind::SwiGLUFwd;
+    eg.g_out = sptr(st, L4D_STASH_GATE);
+    eg.u_out = sptr(st, L4D_STASH_UP);
+    eg.act_out = sptr(st, L4D_STASH_ACT);
+    eg.prod_out = sptr(st, L4D_STASH_PROD);
+    eg.f = (int32_t)x.f_t;
+    Operand bgu{RowSrc::plain(w->gate_up, x.h), (int32_t)(2 * x.f_t), (int32_t)x.f_t, x.f_t};
+    if ((r = run_gemm("gemm_gate_up", s, tok, 2 * x.f_t, x.h, op(gathered(sptr(st, L4D_STASH_XN2), pi.sp_peer_xn2, x), tok),
+                      Layout::KC, bgu, Layout::KC, eg)))
+      return r;
+    // y = h1 + prod W_down^T
+    if ((r = run_gemm("gemm_down", s, tok, x.h, x.f_t, op(RowSrc::plain(sptr(st, L4D_STASH_PROD), x.f_t), tok),
+                      Layout::KC, op(RowSrc::plain(w->down, x.f_t), x.h), Layout::KC,
+                      epi_residual(x, static_cast<uint16_t*>(y), sptr(st, L4D_STASH_H1), pi.sp_peer_ffn, ffn_send))))
+      return r;
+    return L4D_OK;
+  };
+  rc = body();
+  if (rc) {
+    l4d_stash_release(A, st);
+    return rc;
+  }
+  *stash_out = st;
+  return L4D_OK;
+}
+
+// ============================================================== layer backward
+
+extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const l4d_layer_weights* w,
+                               const l4d_peer_inputs* peers, const l4d_peer_outputs* sends, l4d_stash* st,
+                               const void* dy, void* dx, const l4d_layer_grads* dw, void* d_remote_k,
+                               void* d_remote_v, l4d_arena* A, void* stream_ptr) {
+  Shard x;
+  int rc = make_shard(m, p, &x);
+  if (rc) return rc;
+  if (!w || !w->norm1 || !w->qkv || !w->o || !w->norm2 || !w->gate_up || !w->down)
+    return fail(L4D_EINVAL, "all six weights are required");
+  if (!dw || !dw->norm1 || !dw->qkv || !dw->o || !dw->norm2 || !dw->gate_up || !dw->down)
+    return fail(L4D_EINVAL, "all six gradient accumulators are required");
+  if (!st || !A || !dy || !dx) return fail(L4D_EINVAL, "stash, arena, dy and dx are required");
+  if (st->arena != A || !A->live.count(st)) return fail(L4D_EINVAL, "stash does not belong to this arena");
+  const Shard& sx = st->shape;
+  if (sx.h != x.h || sx.a != x.a || sx.k != x.k || sx.f != x.f || sx.s != x.s || sx.b != x.b || sx.t != x.t ||
+      sx.c != x.c || sx.tr != x.tr || sx.cr != x.cr)
+    return fail(L4D_EINVAL, "stash was made for another shape");
+  if (x.c > 1 && (!d_remote_k || !d_remote_v)) return fail(L4D_EINVAL, "cp > 1 needs d_remote_k and d_remote_v");
+  if ((rc = check_peers(x, peers, true))) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream_ptr);
+
+  const BwdWs plan = plan_bwd(x, sends);
+  Workspace ws;
+  if ((rc = take_ws(A, plan.total, ws))) return rc;
+  uint8_t* wsb = reinterpret_cast<uint8_t*>(A->base + ws.off);
+  auto W = [&](uint64_t off) { return reinterpret_cast<uint16_t*>(wsb + off); };
+  float2* rope = reinterpret_cast<float2*>(wsb + plan.rope);
+  uint16_t *dgu = W(plan.dgu), *dxn2 = W(plan.dxn2), *dh1 = W(plan.dh1), *dctx = W(plan.dctx);
+  uint16_t *dqkv = W(plan.dqkv), *dxn1 = W(plan.dxn1);
+  float* delta = reinterpret_cast<float*>(wsb + plan.delta);
+  float* partial = reinterpret_cast<float*>(wsb + plan.partial);
+  const l4d_peer_inputs none{};
+  const l4d_peer_inputs& pi = peers ? *peers : none;
+  void* dxn2_send = (sends && sends->dxn2_partial) ? sends->dxn2_partial : (void*)W(plan.dxn2_send);
+  void* dxn1_send = (sends && sends->dxn1_partial) ? sends->dxn1_partial : (void*)W(plan.dxn1_send);
+  const int64_t tok = x.b * x.s_c, nq = x.a_t * x.d, qc = qkv_cols(x), rows_sp = x.b * x.s_sp;
+  const int32_t npart = rmsnorm_bwd_partials(rows_sp);
+
+  auto body = [&]() -> int {
+    int r;
+    if ((r = launch("rope_table", s, [&] { return rope_table(rope, x.qmap, (int32_t)x.s_c, (int32_t)x.d, x.base, s); })))
+      return r;
+    const RowSrc dy_full = gathered(dy, pi.sp_peer_dy, x);
+    // d(prod) = dy_full W_down, consumed by the SwiGLU backward in the epilogue
+    EpiParams es{};
+    es.kind = EpiKind::SwiGLUBwd;
+    es.g_in = sptr(st, L4D_STASH_GATE);
+    es.u_in = sptr(st, L4D_STASH_UP);
+    es.act_in = sptr(st, L4D_STASH_ACT);
+    es.dgu = dgu;
+    es.f = (int32_t)x.f_t;
+    if ((r = run_gemm("gemm_down_dx", s, tok, x.f_t, x.h, op(dy_full, tok), Layout::KC,
+                      op(RowSrc::plain(w->down, x.f_t), x.f_t), Layout::MN, es)))
+      return r;
+    // dW_down += dy_full^T prod
+    if ((r = run_gemm("gemm_down_dw", s, x.h, x.f_t, tok, op(dy_full, x.h), Layout::MN,
+                      op(RowSrc::plain(sptr(st, L4D_STASH_PROD), x.f_t), x.f_t), Layout::MN, epi_acc(dw->down, x.f_t))))
+      return r;
+    // d(xn2) = dGU W_gu (own rows + receipt; peers' rows sent)
+    if ((r = run_gemm("gemm_gate_up_dx", s, tok, x.h, 2 * x.f_t, op(RowSrc::plain(dgu, 2 * x.f_t), tok), Layout::KC,
+                      op(RowSrc::plain(w->gate_up, x.h), x.h), Layout::MN,
+                      epi_residual(x, dxn2, nullptr, pi.sp_peer_dxn2, dxn2_send))))
+      return r;
+    const RowSrc xn2_full = gathered(sptr(st, L4D_STASH_XN2), pi.sp_peer_xn2, x);
+    if ((r = run_gemm("gemm_gate_up_dw", s, 2 * x.f_t, x.h, tok, op(RowSrc::plain(dgu, 2 * x.f_t), 2 * x.f_t),
+                      Layout::MN, op(xn2_full, x.h), Layout::MN, epi_acc(dw->gate_up, x.h))))
+      return r;
+    // norm-2 backward + residual
+    if ((r = launch("rmsnorm_bwd", s, [&] {
+           return rmsnorm_bwd(sptr(st, L4D_STASH_H1), static_cast<const uint16_t*>(w->norm2), dxn2,
+                              static_cast<const uint16_t*>(dy), dh1, partial, npart, rows_sp, (int32_t)x.h, x.eps, s);
+         })))
+      return r;
+    if ((r = launch("reduce_gain", s, [&] { return reduce_rows_add(partial, npart, (int32_t)x.h, dw->norm2, s); })))
+      return r;
+    // attention output projection
+    const RowSrc dh1_full = gathered(dh1, pi.sp_peer_dh1, x);
+    if ((r = run_gemm("gemm_o_dx", s, tok, nq, x.h, op(dh1_full, tok), Layout::KC, op(RowSrc::plain(w->o, nq), nq),
+                      Layout::MN, epi_store(dctx, nq))))
+      return r;
+    if ((r = run_gemm("gemm_o_dw", s, x.h, nq, tok, op(dh1_full, x.h), Layout::MN,
+                      op(RowSrc::plain(sptr(st, L4D_STASH_CTX), nq), nq), Layout::MN, epi_acc(dw->o, nq))))
+      return r;
+    // attention backward -> dQKV (inverse RoPE applied), remote dK/dV
+    AttnParams ap = attn_params(x);
+    ap.q = sptr(st, L4D_STASH_Q);
+    ap.o = sptr(st, L4D_STASH_CTX);
+    ap.lse = sptr<float>(st, L4D_STASH_LSE);
+    ap.dout = dctx;
+    ap.delta = delta;
+    ap.dq = dqkv;
+    ap.dq_ld = qc;
+    ap.rope = rope;
+    key_segments(x, ap, sptr(st, L4D_STASH_K), sptr(st, L4D_STASH_V), static_cast<const uint16_t*>(pi.remote_k),
+                 static_cast<const uint16_t*>(pi.remote_v), dqkv, static_cast<uint16_t*>(d_remote_k),
+                 static_cast<uint16_t*>(d_remote_v), static_cast<const uint16_t*>(pi.cp_peer_dk),
+                 static_cast<const uint16_t*>(pi.cp_peer_dv));
+    if ((r = launch("attn_bwd", s, [&] { return attn_bwd(ap, s); }))) return r;
+    // QKV projection
+    if ((r = run_gemm("gemm_qkv_dx", s, tok, x.h, qc, op(RowSrc::plain(dqkv, qc), tok), Layout::KC,
+                      op(RowSrc::plain(w->qkv, x.h), x.h), Layout::MN,
+                      epi_residual(x, dxn1, nullptr, pi.sp_peer_dxn1, dxn1_send))))
+      return r;
+    const RowSrc xn1_full = gathered(sptr(st, L4D_STASH_XN1), pi.sp_peer_xn1, x);
+    if ((r = run_gemm("gemm_qkv_dw", s, qc, x.h, tok, op(RowSrc::plain(dqkv, qc), qc), Layout::MN, op(xn1_full, x.h),
+                      Layout::MN, epi_acc(dw->qkv, x.h))))
+      return r;
+    // norm-1 backward + residual
+    if ((r = launch("rmsnorm_bwd", s, [&] {
+           return rmsnorm_bwd(sptr(st, L4D_STASH_X), static_cast<const uint16_t*>(w->norm1), dxn1, dh1,
+                              static_cast<uint16_t*>(dx), partial, npart, rows_sp, (int32_t)x.h, x.eps, s);
+         })))
+      return r;
+    if ((r = launch("reduce_gain", s, [&] { return reduce_rows_add(partial, npart, (int32_t)x.h, dw->norm1, s); })))
+      return r;
+    return L4D_OK;
+  };
+  rc = body();
+  if (rc) return rc;
+  return l4d_stash_release(A, st);
+}
+
+// ============================================================== LM head
+
+extern "C" int lm_head_xent(int64_t n, int64_t h, int64_t v_t, int64_t v0, const void* hidden, const void* w_lm,
+                            const int64_t* targets, const float* peer_lse, const float* peer_z, float grad_scale,
+                            float* loss, void* d_hidden, float* d_w, l4d_arena* A, void* stream_ptr) {
+  if (n < 0 || h <= 0 || v_t <= 0 || v0 < 0) return fail(L4D_EINVAL, "bad LM-head sizes");
+  if (h % 8 || v_t % 8) return fail(L4D_EINVAL, "hidden and vocab shard must be multiples of 8");
+  if (n * v_t > ((int64_t)1 << 40) || n > INT32_MAX || v_t > INT32_MAX) return fail(L4D_EINVAL, "problem too large");
+  if (!hidden || !w_lm || !targets || !loss || !d_hidden || !d_w || !A)
+    return fail(L4D_EINVAL, "hidden, w_lm, targets, loss, d_hidden, d_w_lm and arena are required");
+  if ((peer_lse == nullptr) != (peer_z == nullptr))
+    return fail(L4D_EINVAL, "peer_lse and peer_target_logit go together");
+  if (n == 0) return L4D_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream_ptr);
+  Workspace ws;
+  int rc = take_ws(A, (uint64_t)n * v_t * 2, ws);
+  if (rc) return rc;
+  uint16_t* logits = reinterpret_cast<uint16_t*>(A->base + ws.off);
+  if ((rc = run_gemm("gemm_lm_logits", s, n, v_t, h, op(RowSrc::plain(hidden, h), n), Layout::KC,
+                     op(RowSrc::plain(w_lm, h), v_t), Layout::KC, epi_store(logits, v_t))))
+    return rc;
+  if ((rc = launch("xent_rows", s, [&] {
+         return xent_rows(logits, n, (int32_t)v_t, v0, targets, peer_lse, peer_z, grad_scale, loss, logits, s);
+       })))
+    return rc;
+  if ((rc = run_gemm("gemm_lm_dx", s, n, h, v_t, op(RowSrc::plain(logits, v_t), n), Layout::KC,
+                     op(RowSrc::plain(w_lm, h), h), Layout::MN, epi_store(d_hidden, h))))
+    return rc;
+  return run_gemm("gemm_lm_dw", s, v_t, h, n, op(RowSrc::plain(logits, v_t), v_t), Layout::MN,
+                  op(RowSrc::plain(hidden, h), h), Layout::MN, epi_acc(d_w, h));
+}

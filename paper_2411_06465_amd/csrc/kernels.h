@@ -1,0 +1,164 @@
+// Internal interface between the C ABI (abi.cpp) and the HIP kernels.
+// Every launcher enqueues on `stream` and returns the launch status.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace l4d {
+
+// Rows of a token-major activation that may be split between this rank's own
+// sequence-parallel rows and the rows the all-gather brings from the peers.
+// Logical row m (0 <= m < b*s_c) lives at own + (...)*ld when its in-sequence
+// index i = m % s_c falls in [r*s_sp, (r+1)*s_sp), else in peer.
+// With t == 1 (or peer == nullptr) it is simply base + m*ld.
+struct RowSrc {
+  const uint16_t* own;
+  const uint16_t* peer;
+  int64_t ld;     // elements between consecutive rows
+  int32_t s_c;    // rows per batch element of the gathered view
+  int32_t s_sp;   // own rows per batch element
+  int32_t r;      // own slot
+  int32_t t;      // slots (1 = not split)
+
+  __host__ __device__ static RowSrc plain(const void* p, int64_t ld) {
+    return RowSrc{static_cast<const uint16_t*>(p), nullptr, ld, 1, 1, 0, 1};
+  }
+  __device__ inline const uint16_t* row(int64_t m) const {
+    if (t == 1) return own + m * ld;
+    int64_t bi = m / s_c;
+    int32_t i = static_cast<int32_t>(m - bi * s_c);
+    int32_t lo = r * s_sp;
+    if (i >= lo && i < lo + s_sp) return own + (bi * s_sp + (i - lo)) * ld;
+    int32_t pi = i < lo ? i : i - s_sp;
+    return peer + (bi * static_cast<int64_t>(t - 1) * s_sp + pi) * ld;
+  }
+};
+
+// One GEMM operand.  "kc" (k-contiguous): element (x, k) at src.row(x)[k].
+// "mn" (mn-contiguous): element (x, k) at src.row(k)[x].
+// split: (k-contiguous B only) tile rows [0,128) of N-tile j come from rows
+// j*128 + [0,128) and tile rows [128,256) from split_off + j*128 + [0,128);
+// rows with j*128 + i >= split_rows are zero.  Used to interleave the gate
+// and up halves of a fused [gate; up] weight so one tile holds both.
+struct Operand {
+  RowSrc src;
+  int32_t rows;        // extent of the non-k index (M for A, N for B) in storage
+  int32_t split_rows;  // 0 = no split
+  int64_t split_off;
+};
+
+enum class Layout { KC, MN };
+
+// ---------------------------------------------------------------- epilogues
+// Every GEMM hands its fp32 tile to one of these, as 8-column vectors.
+
+enum class EpiKind {
+  StoreBF16,    // C (bf16) = acc, row-major with ldc
+  AccF32,       // C (f32) += acc
+  QkvRope,      // split [Q|K|V] columns, RoPE on Q and K, bf16
+  ResidualSP,   // own rows: bf16(acc + resid + receipt); peer rows: bf16(acc) -> send buffer
+  SwiGLUFwd,    // gate/up tile pairs -> G, U, act, prod (bf16)
+  SwiGLUBwd     // acc = d(prod) -> dG, dU from the stashed G, U, act
+};
+
+struct EpiParams {
+  EpiKind kind;
+  void* c;              // StoreBF16 / AccF32 output
+  int64_t ldc;
+  // QkvRope
+  uint16_t *q, *k, *v;
+  int32_t nq, nk;       // columns of Q and of K (= of V)
+  const float2* rope;   // [tokens_per_batch][d_h/2] (cos, sin) by local row
+  int32_t d_h;
+  // ResidualSP (rows in the gathered view; own rows mapped like RowSrc)
+  uint16_t* own_out;    // [b*s_sp][ldc]
+  const uint16_t* resid;    // may be null
+  const uint16_t* receipt;  // may be null
+  uint16_t* send;       // [b*(t-1)*s_sp][ldc]
+  int32_t s_c, s_sp, r, t;
+  // SwiGLUFwd / SwiGLUBwd: [tokens][f] tensors, f = split_rows of B
+  uint16_t *g_out, *u_out, *act_out, *prod_out;
+  const uint16_t *g_in, *u_in, *act_in;
+  uint16_t* dgu;        // [tokens][2f] : dG columns [0,f), dU columns [f,2f)
+  int32_t f;
+};
+
+struct GemmParams {
+  int32_t M, N, K;
+  Operand A, B;
+  EpiParams epi;
+};
+
+hipError_t gemm(const GemmParams& p, Layout la, Layout lb, hipStream_t stream);
+
+// ---------------------------------------------------------------- row-wise kernels
+
+// y = bf16(gain * x * rsqrt(mean(x^2) + eps)), one row of h per wave.
+hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* gain, uint16_t* y, int64_t rows,
+                       int32_t h, float eps, hipStream_t stream);
+// dx = bf16(dres + d rmsnorm/dx . dy);  partial[blk][h] = sum over the block's rows of dy*xhat.
+hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const uint16_t* dy,
+                       const uint16_t* dres, uint16_t* dx, float* partial, int32_t n_partial,
+                       int64_t rows, int32_t h, float eps, hipStream_t stream);
+// out[j] += sum_i partial[i][j]
+hipError_t reduce_rows_add(const float* partial, int32_t n_partial, int32_t h, float* out,
+                           hipStream_t stream);
+int32_t rmsnorm_bwd_partials(int64_t rows);
+
+// cos/sin table for RoPE: tab[i][j] = (cos, sin)(pos_i * base^(-2j/d_h)), computed in fp64.
+struct ChunkMap {          // local row -> global position
+  int32_t n_chunks;        // 1 or 2
+  int32_t chunk_len;
+  int32_t chunk_id[2];
+};
+hipError_t rope_table(float2* tab, ChunkMap map, int32_t rows, int32_t d_h, float base,
+                      hipStream_t stream);
+
+// ---------------------------------------------------------------- attention
+
+// A run of keys with consecutive global positions.
+struct KvSeg {
+  const uint16_t* k;   // token 0 of the run: [tokens][ld], head hk at column hk*d_h
+  const uint16_t* v;
+  int64_t ld, bstride;     // row and batch strides of k, v, rk, rv (elements)
+  uint16_t* dk;        // backward outputs, may be null in the forward
+  uint16_t* dv;
+  int64_t d_ld, d_bstride; // row and batch strides of dk, dv
+  const uint16_t* rk;  // receipts added before storing dk/dv (null = none)
+  const uint16_t* rv;
+  int32_t n;           // tokens
+  int32_t pos0;        // global position of token 0
+  int32_t rope;        // 1: apply the inverse RoPE to dk (local keys)
+  int32_t rope_row0;   // row of token 0 in the RoPE table
+};
+constexpr int kMaxSeg = 8;
+
+struct AttnParams {
+  int32_t b, a_t, k_t, d_h;
+  int32_t n_q;                 // local query rows per batch element
+  int64_t q_ld, q_bstride;     // strides of q, o, dout (elements)
+  const uint16_t* q;           // [b][n_q][a_t*d_h]
+  uint16_t* o;                 // ctx, same layout
+  float* lse;                  // [b][a_t][n_q], natural log
+  ChunkMap qmap;               // local query row -> global position
+  int32_t n_seg;
+  KvSeg seg[kMaxSeg];
+  float scale;                 // 1/sqrt(d_h)
+  // backward
+  const uint16_t* dout;        // dctx
+  float* delta;                // [b][a_t][n_q]
+  uint16_t* dq;                // [b][n_q][dq_ld] at column h*d_h, inverse RoPE applied
+  int64_t dq_ld;
+  const float2* rope;          // table used by the inverse RoPE
+};
+
+hipError_t attn_fwd(const AttnParams& p, hipStream_t stream);
+hipError_t attn_bwd(const AttnParams& p, hipStream_t stream);
+
+// ---------------------------------------------------------------- cross-entropy
+
+hipError_t xent_rows(const uint16_t* logits, int64_t n, int32_t v_t, int64_t v0,
+                     const int64_t* targets, const float* peer_lse, const float* peer_z,
+                     float grad_scale, float* loss, uint16_t* dlogits, hipStream_t stream);
+
+}  // namespace l4d

@@ -1,0 +1,303 @@
+// Memory-bound row kernels: RMSNorm forward/backward, the gain-gradient
+// reduction, the RoPE angle table and the vocabulary-parallel cross-entropy.
+// One wave (64 lanes) owns one row; every global access is a 16-byte vector.
+#include <math.h>
+
+#include "kernels.h"
+
+namespace l4d {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+__device__ __forceinline__ void unpack8(u32x4 u, float* v) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(u[i] << 16);
+    v[2 * i + 1] = __uint_as_float(u[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ u32x4 pack8(const float* v) {
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r[i] = (uint32_t)f2bf(v[2 * i]) | ((uint32_t)f2bf(v[2 * i + 1]) << 16);
+  return r;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+constexpr int kMaxChunks = 16;   // h <= 64 lanes * 16 chunks * 8 = 8192
+
+// ------------------------------------------------------------------ RMSNorm
+
+__global__ void __launch_bounds__(256) rmsnorm_fwd_kernel(const uint16_t* __restrict__ x,
+                                                          const uint16_t* __restrict__ gain,
+                                                          uint16_t* __restrict__ y, int64_t rows,
+                                                          int32_t h, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int nch = h / 8;
+  const u32x4* xr = reinterpret_cast<const u32x4*>(x + row * h);
+  u32x4 v[kMaxChunks];
+  float ss = 0.f;
+#pragma unroll
+  for (int it = 0; it < kMaxChunks; ++it) {
+    const int c = lane + 64 * it;
+    if (c < nch) {
+      v[it] = xr[c];
+      float f[8];
+      unpack8(v[it], f);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ss += f[j] * f[j];
+    }
+  }
+  const float rstd = rsqrtf(wave_sum(ss) / h + eps);
+  const u32x4* gr = reinterpret_cast<const u32x4*>(gain);
+  u32x4* yr = reinterpret_cast<u32x4*>(y + row * h);
+#pragma unroll
+  for (int it = 0; it < kMaxChunks; ++it) {
+    const int c = lane + 64 * it;
+    if (c < nch) {
+      float f[8], g[8];
+      unpack8(v[it], f);
+      unpack8(gr[c], g);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) f[j] = f[j] * rstd * g[j];
+      yr[c] = pack8(f);
+    }
+  }
+}
+
+// Grid-stride over rows; each block keeps per-column partial sums of dy*xhat
+// and writes them to partial[blockIdx.x][h].
+__global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ gain, const uint16_t* __restrict__ dy,
+    const uint16_t* __restrict__ dres, uint16_t* __restrict__ dx, float* __restrict__ partial,
+    int64_t rows, int32_t h, float eps) {
+  __shared__ float red[4][8192 / 4];   // per-wave partials, reduced in two halves
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nch = h / 8;
+  float acc[kMaxChunks][8];
+#pragma unroll
+  for (int it = 0; it < kMaxChunks; ++it)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[it][j] = 0.f;
+  const u32x4* gr = reinterpret_cast<const u32x4*>(gain);
+  for (int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wave; row < rows;
+       row += static_cast<int64_t>(gridDim.x) * 4) {
+    const u32x4* xr = reinterpret_cast<const u32x4*>(x + row * h);
+    const u32x4* dr = reinterpret_cast<const u32x4*>(dy + row * h);
+    u32x4 xv[kMaxChunks], dv[kMaxChunks];
+    float ss = 0.f, dot = 0.f;
+#pragma unroll
+    for (int it = 0; it < kMaxChunks; ++it) {
+      const int c = lane + 64 * it;
+      if (c < nch) {
+        xv[it] = xr[c];
+        dv[it] = dr[c];
+        float f[8], d[8], g[8];
+        unpack8(xv[it], f);
+        unpack8(dv[it], d);
+        unpack8(gr[c], g);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          ss += f[j] * f[j];
+          dot += g[j] * d[j] * f[j];
+        }
+      }
+    }
+    const float rstd = rsqrtf(wave_sum(ss) / h + eps);
+    // mean over the row of (gain*dy) * xhat
+    const float c_mean = wave_sum(dot) * rstd / h;
+    const u32x4* rr = dres ? reinterpret_cast<const u32x4*>(dres + row * h) : nullptr;
+    u32x4* out = reinterpret_cast<u32x4*>(dx + row * h);
+#pragma unroll
+    for (int it = 0; it < kMaxChunks; ++it) {
+      const int c = lane + 64 * it;
+      if (c < nch) {
+        float f[8], d[8], g[8], r[8];
+        unpack8(xv[it], f);
+        unpack8(dv[it], d);
+        unpack8(gr[c], g);
+        if (rr) unpack8(rr[c], r);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float xh = f[j] * rstd;
+          acc[it][j] += d[j] * xh;
+          float v = rstd * (g[j] * d[j] - xh * c_mean);
+          r[j] = rr ? r[j] + v : v;
+        }
+        out[c] = pack8(r);
+      }
+    }
+  }
+  // block reduction of acc over the 4 waves, in chunks of h/4 columns
+  for (int part = 0; part < 4; ++part) {
+    const int lo = part * (h / 4), hi = lo + h / 4;
+#pragma unroll
+    for (int it = 0; it < kMaxChunks; ++it) {
+      const int c = lane + 64 * it;
+      if (c < nch) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int col = c * 8 + j;
+          if (col >= lo && col < hi) red[wave][col - lo] = acc[it][j];
+        }
+      }
+    }
+    __syncthreads();
+    for (int col = threadIdx.x; col < h / 4; col += 256)
+      partial[static_cast<int64_t>(blockIdx.x) * h + lo + col] =
+          red[0][col] + red[1][col] + red[2][col] + red[3][col];
+    __syncthreads();
+  }
+}
+
+__global__ void reduce_rows_add_kernel(const float* __restrict__ partial, int32_t n_partial, int32_t h,
+                                       float* __restrict__ out) {
+  const int col = blockIdx.x * blockDim.x + threadIdx.x;
+  if (col >= h) return;
+  float s = 0.f;
+  for (int i = 0; i < n_partial; ++i) s += partial[static_cast<int64_t>(i) * h + col];
+  out[col] += s;
+}
+
+// ------------------------------------------------------------------ RoPE table
+
+__global__ void rope_table_kernel(float2* tab, ChunkMap map, int32_t rows, int32_t d_h, double log_base) {
+  const int half = d_h / 2;
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= static_cast<int64_t>(rows) * half) return;
+  const int i = static_cast<int>(idx / half), j = static_cast<int>(idx % half);
+  const int ci = i / map.chunk_len;
+  const int64_t pos = static_cast<int64_t>(map.chunk_id[ci]) * map.chunk_len + (i - ci * map.chunk_len);
+  const double ang = static_cast<double>(pos) * exp(-2.0 * j / d_h * log_base);
+  double s, c;
+  sincos(ang, &s, &c);
+  tab[idx] = make_float2(static_cast<float>(c), static_cast<float>(s));
+}
+
+// ------------------------------------------------------------------ cross-entropy
+// One 256-thread block per token row of bf16 logits [n][v_t] (v_t % 8 == 0).
+
+__global__ void __launch_bounds__(256) xent_rows_kernel(
+    const uint16_t* __restrict__ logits, int32_t v_t, int64_t v0, const int64_t* __restrict__ targets,
+    const float* __restrict__ peer_lse, const float* __restrict__ peer_z, float grad_scale,
+    float* __restrict__ loss, uint16_t* __restrict__ dlogits) {
+  __shared__ float red[4];
+  __shared__ float bcast;
+  const int64_t row = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const u32x4* lr = reinterpret_cast<const u32x4*>(logits + row * v_t);
+  const int nch = v_t / 8;
+  float mx = -INFINITY;
+  for (int c = threadIdx.x; c < nch; c += 256) {
+    float f[8];
+    unpack8(lr[c], f);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) mx = fmaxf(mx, f[j]);
+  }
+  mx = wave_max(mx);
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  float se = 0.f;
+  for (int c = threadIdx.x; c < nch; c += 256) {
+    float f[8];
+    unpack8(lr[c], f);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) se += __expf(f[j] - mx);
+  }
+  se = wave_sum(se);
+  if (lane == 0) red[wave] = se;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float lse = mx + logf(red[0] + red[1] + red[2] + red[3]);
+    if (peer_lse) {
+      const float p = peer_lse[row];
+      const float hi = fmaxf(lse, p), lo = fminf(lse, p);
+      lse = hi + log1pf(__expf(lo - hi));
+    }
+    const int64_t tgt = targets[row] - v0;
+    float z;
+    if (tgt >= 0 && tgt < v_t) z = __uint_as_float(static_cast<uint32_t>(logits[row * v_t + tgt]) << 16);
+    else z = peer_z ? peer_z[row] : 0.f;
+    loss[row] = lse - z;
+    bcast = lse;
+  }
+  __syncthreads();
+  const float lse = bcast;
+  const int64_t tgt = targets[row] - v0;
+  u32x4* dr = reinterpret_cast<u32x4*>(dlogits + row * v_t);
+  for (int c = threadIdx.x; c < nch; c += 256) {
+    float f[8];
+    unpack8(lr[c], f);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      float g = __expf(f[j] - lse);
+      if (c * 8 + j == tgt) g -= 1.0f;
+      f[j] = g * grad_scale;
+    }
+    dr[c] = pack8(f);
+  }
+}
+
+}  // namespace
+
+hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* gain, uint16_t* y, int64_t rows, int32_t h,
+                       float eps, hipStream_t stream) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_fwd_kernel, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream,
+                     x, gain, y, rows, h, eps);
+  return hipGetLastError();
+}
+
+int32_t rmsnorm_bwd_partials(int64_t rows) {
+  int64_t blocks = (rows + 3) / 4;
+  return static_cast<int32_t>(blocks < 256 ? blocks : 256);
+}
+
+hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const uint16_t* dy, const uint16_t* dres,
+                       uint16_t* dx, float* partial, int32_t n_partial, int64_t rows, int32_t h, float eps,
+                       hipStream_t stream) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_bwd_kernel, dim3(n_partial), dim3(256), 0, stream, x, gain, dy, dres, dx,
+                     partial, rows, h, eps);
+  return hipGetLastError();
+}
+
+hipError_t reduce_rows_add(const float* partial, int32_t n_partial, int32_t h, float* out, hipStream_t stream) {
+  hipLaunchKernelGGL(reduce_rows_add_kernel, dim3((h + 255) / 256), dim3(256), 0, stream, partial, n_partial,
+                     h, out);
+  return hipGetLastError();
+}
+
+hipError_t rope_table(float2* tab, ChunkMap map, int32_t rows, int32_t d_h, float base, hipStream_t stream) {
+  const int64_t n = static_cast<int64_t>(rows) * (d_h / 2);
+  hipLaunchKernelGGL(rope_table_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream,
+                     tab, map, rows, d_h, log(static_cast<double>(base)));
+  return hipGetLastError();
+}
+
+hipError_t xent_rows(const uint16_t* logits, int64_t n, int32_t v_t, int64_t v0, const int64_t* targets,
+                     const float* peer_lse, const float* peer_z, float grad_scale, float* loss,
+                     uint16_t* dlogits, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(xent_rows_kernel, dim3(static_cast<unsigned>(n)), dim3(256), 0, stream, logits, v_t, v0,
+                     targets, peer_lse, peer_z, grad_scale, loss, dlogits);
+  return hipGetLastError();
+}
+
+}  // namespace l4d

@@ -1,0 +1,191 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library is loaded and driven through ctypes, but only its host logic runs:
+symbol exports, the memory estimate, the arena / stash bookkeeping and the
+argument validation.  Nothing here launches a kernel; arenas are created over
+a fake device address that the host code never dereferences.
+"""
+import ctypes as C
+import json
+import os
+import re
+
+import pytest
+
+import paper_2411_06465_amd as L
+from oracle import memory as M
+from workloads import LAYER_WORKLOADS, TINY, LLAMA2_7B, LLAMA3_8B_TP2CP2, LLAMA3_70B_TP8
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "l4d.h")
+FAKE_BASE = 1 << 40            # never dereferenced by the host code
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH), reason="libl4d.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\**(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert "llama_layer_fwd" in names and "mem_estimate" in names and "lm_head_xent" in names
+    lib = C.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def model_par(w, **over):
+    d = dict(w.model())
+    d.update(over)
+    p = dict(w.parallel())
+    p.update({k: v for k, v in over.items() if k in p})
+    return L.make_model(**d), L.make_parallel(**p)
+
+
+# ------------------------------------------------------------------ memory estimate
+
+ARCH = {"llama-3.1-8b": (4096, 32, 8, 14336, 32, 128256), "llama-3.1-70b": (8192, 64, 8, 28672, 80, 128256)}
+
+
+def test_mem_estimate_equals_oracle_on_every_paper_cell():
+    cells = json.load(open(os.path.join(ROOT, "tests", "golden", "paper_memory_tables.json")))["cells"]
+    for c in cells:
+        h, a, k, f, Lyr, v = ARCH[c["model"]]
+        d = c["n_gpus"] // (c["tp"] * c["cp"] * c["pp"])
+        got = L.mem_estimate(L.make_model(h, a, k, f, Lyr, v),
+                             L.make_parallel(c["seq"], c["mbs"], c["tp"], c["cp"], c["pp"], d))
+        want = M.estimate(h, a, k, f, Lyr, v, s=c["seq"], b=c["mbs"], t=c["tp"], c=c["cp"], p=c["pp"], d=d)
+        assert got["params_per_gpu"] == want["params"]
+        assert got["weight_bytes"] == want["weight"]
+        assert got["grad_bytes"] == want["grad"]
+        assert got["optim_bytes"] == want["optim"]
+        assert got["act_bytes_per_layer"] == want["act_layer"]
+        assert got["act_bytes"] == want["act"]
+        assert got["total_bytes"] == want["total"]
+        assert got["inexact"] == 0
+
+
+@pytest.mark.parametrize("w", list(LAYER_WORKLOADS.values()), ids=lambda w: w.name)
+def test_mem_estimate_equals_oracle_on_workloads(w):
+    got = L.mem_estimate(*model_par(w))
+    want = M.estimate(w.hidden, w.n_heads, w.n_kv_heads, w.ffn, w.n_layers, w.vocab, s=w.seq,
+                      b=w.micro_batch, t=w.tp, c=w.cp, p=w.pp, d=w.dp)
+    assert got["total_bytes"] == want["total"] and got["act_bytes_per_layer"] == want["act_layer"]
+
+
+def test_mem_estimate_pins():
+    # Appendix A.1, 70B (8,1,8,1) on 256 GPUs: 35.88 GiB; Sec. 4.2.1: 89.95 GiB
+    g = L.mem_estimate(*model_par(LLAMA3_70B_TP8))
+    assert g["total_bytes"] == 38_525_370_368
+    g = L.mem_estimate(L.make_model(4096, 32, 8, 14336, 32, 128256), L.make_parallel(8192, 1, 1, 2, 1, 2))
+    assert round(g["total_bytes"] / 2 ** 30, 2) == 89.95
+
+
+def test_mem_estimate_flags_fractional_terms():
+    # d*c = 3 does not divide 12 Psi for this tiny model: rounded up and flagged
+    g = L.mem_estimate(L.make_model(8, 1, 1, 8, 1, 8), L.make_parallel(8, 1, 1, 1, 1, 7))
+    psi = M.params_per_gpu(8, 1, 1, 8, 1, 8, 1, 1)
+    assert g["params_per_gpu"] == psi
+    assert g["inexact"] == (0 if (12 * psi) % 7 == 0 else 1)
+
+
+@pytest.mark.parametrize("bad", [dict(n_heads=3), dict(n_kv_heads=3), dict(tp=3), dict(cp=3), dict(pp=3),
+                                 dict(tp_rank=2), dict(cp_rank=-1), dict(ffn=31), dict(seq=0)])
+def test_mem_estimate_rejects_bad_layouts(bad):
+    base = dict(hidden=64, n_heads=4, n_kv_heads=2, ffn=32, n_layers=4, vocab=16, seq=16, tp=2, cp=2, pp=2)
+    base.update(bad)
+    m = L.make_model(**base)
+    p = L.make_parallel(**base)
+    with pytest.raises(L.L4DError) as e:
+        L.mem_estimate(m, p)
+    assert e.value.code == L.L4D_EINVAL
+
+
+# ------------------------------------------------------------------ stash accounting
+
+@pytest.mark.parametrize("w", list(LAYER_WORKLOADS.values()), ids=lambda w: w.name)
+def test_stash_bytes_equal_the_activation_formula(w):
+    m, p = model_par(w)
+    want = M.act_bytes_per_layer(w.hidden, w.n_heads, w.n_kv_heads, w.ffn, w.seq, w.micro_batch, w.tp, w.cp)
+    a = L.Arena(FAKE_BASE, 1 << 40)
+    st = L.l4d_stash_reserve(a, m, p)
+    b = st.bytes()
+    assert b["formula"] == want == L.mem_estimate(m, p)["act_bytes_per_layer"]
+    assert b["aux"] == 4 * w.micro_batch * w.a_t * w.s_c      # FlashAttention LSE, counted as zero
+    # every tensor inside the arena block, disjoint
+    spans = sorted(st.tensor(i) for i in range(len(L.STASH_NAMES)))
+    for (p0, n0), (p1, _) in zip(spans, spans[1:]):
+        assert p0 + n0 <= p1
+    assert spans[0][0] >= FAKE_BASE
+    st.release()
+    assert a.stats()["in_use"] == 0
+    a.destroy()
+
+
+def test_stash_reserve_fails_with_enomem_exactly_at_capacity():
+    m, p = model_par(TINY)
+    probe = L.Arena(FAKE_BASE, 1 << 30)
+    st = L.l4d_stash_reserve(probe, m, p)
+    need = probe.stats()["in_use"]
+    st.release()
+    probe.destroy()
+    ok = L.Arena(FAKE_BASE, need)
+    L.l4d_stash_reserve(ok, m, p).release()
+    small = L.Arena(FAKE_BASE, need - 256)
+    with pytest.raises(L.L4DError) as e:
+        L.l4d_stash_reserve(small, m, p)
+    assert e.value.code == L.L4D_ENOMEM
+    assert small.stats()["in_use"] == 0
+
+
+@pytest.mark.parametrize("order", ["fifo", "lifo"])
+def test_arena_release_orders_restore_a_single_free_block(order):
+    # 1F1B keeps up to p micro-batches of stashes alive; release in either order.
+    m, p = model_par(TINY)
+    a = L.Arena(FAKE_BASE, 64 << 20)
+    stashes = [L.l4d_stash_reserve(a, m, p) for _ in range(8)]
+    peak = a.stats()["in_use"]
+    assert peak == 8 * (peak // 8)
+    for st in (stashes if order == "fifo" else stashes[::-1]):
+        st.release()
+    assert a.stats()["in_use"] == 0 and a.stats()["peak"] == peak
+    # coalesced: the whole capacity fits again
+    big = L.Arena(FAKE_BASE, 64 << 20)
+    sts = [L.l4d_stash_reserve(big, m, p) for _ in range(8)]
+    for st in sts:
+        st.release()
+    a.destroy()
+    big.destroy()
+
+
+def test_arena_destroy_refuses_live_stash():
+    m, p = model_par(TINY)
+    a = L.Arena(FAKE_BASE, 64 << 20)
+    st = L.l4d_stash_reserve(a, m, p)
+    with pytest.raises(L.L4DError):
+        a.destroy()
+    st.release()
+    a.destroy()
+
+
+def test_workspace_sizes_are_reported():
+    for w in LAYER_WORKLOADS.values():
+        f, b = L.l4d_layer_workspace_bytes(*model_par(w))
+        assert f > 0 and b > 0
+    assert L.l4d_lm_head_workspace_bytes(8192, 4096, 32064) == 8192 * 32064 * 2
+
+
+def test_layer_calls_validate_before_touching_the_device():
+    m, p = model_par(LLAMA3_8B_TP2CP2)
+    a = L.Arena(FAKE_BASE, 1 << 40)
+    # missing weights -> EINVAL, nothing reserved
+    rc = L.lib().llama_layer_fwd(C.byref(m), C.byref(p), None, None, None, None, None, a.h, C.byref(C.c_void_p()), None)
+    assert rc == L.L4D_EINVAL and a.stats()["in_use"] == 0
+    # head dim 96 unsupported
+    m2 = L.make_model(hidden=96 * 4, n_heads=4, n_kv_heads=4, ffn=64)
+    with pytest.raises(L.L4DError):
+        L.l4d_layer_workspace_bytes(m2, L.make_parallel(64))
+    a.destroy()
