@@ -1,0 +1,288 @@
+"""Benchmark: one GPU's share of a Llama decoder-layer training step.
+
+A step is one pass of the hot path on a fixed synthetic batch: the memory
+estimate (host), the layer forward (which reserves the activation stash) and
+the layer backward (which adds into fp32 weight-gradient accumulators).  The
+headline workload is the Llama-2-7B-shaped layer (h 4096, 32/32 heads,
+FFN 11008, seq 4096, micro-batch 1, TP1 CP1); the other shard shapes
+(Llama-3-8B at TP2 CP2, Llama-3-70B at TP8, the Llama-3-8B LM head at TP4)
+are reported alongside under "other_workloads".
+
+Throughput is model FLOPs (forward GEMMs + causal attention over the
+unmasked query/key pairs, times 3 for forward + backward) per second.  Kernel
+durations come from HIP events that the library records around each launch
+on the launch stream, over the timed steps.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline] [--no-others]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA, published
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E, published
+
+
+# ------------------------------------------------------------------ FLOP / byte accounting
+
+def attn_pairs(w):
+    """Unmasked (query, key) pairs per head for this shard: the local query at
+    global position q sees the q + 1 keys at positions 0..q."""
+    if w.cp == 1:
+        pos = np.arange(w.seq)
+    else:
+        n = w.seq // (2 * w.cp)
+        pos = np.concatenate([np.arange(c * n, (c + 1) * n) for c in (w.cp_rank, 2 * w.cp - 1 - w.cp_rank)])
+    return int(np.sum(pos + 1))
+
+
+def gemm_shapes(w):
+    tok = w.micro_batch * w.s_c
+    h, nq, qc, f = w.hidden, w.a_t * w.d_h, (w.a_t + 2 * w.k_t) * w.d_h, w.f_t
+    return {
+        "gemm_qkv": (tok, qc, h), "gemm_o": (tok, h, nq), "gemm_gate_up": (tok, 2 * f, h), "gemm_down": (tok, h, f),
+        "gemm_down_dx": (tok, f, h), "gemm_down_dw": (h, f, tok), "gemm_gate_up_dx": (tok, h, 2 * f),
+        "gemm_gate_up_dw": (2 * f, h, tok), "gemm_o_dx": (tok, nq, h), "gemm_o_dw": (h, nq, tok),
+        "gemm_qkv_dx": (tok, h, qc), "gemm_qkv_dw": (qc, h, tok),
+    }
+
+
+def layer_flops(w):
+    tok = w.micro_batch * w.s_c
+    h, nq, qc, f = w.hidden, w.a_t * w.d_h, (w.a_t + 2 * w.k_t) * w.d_h, w.f_t
+    gemm_fwd = 2 * tok * (h * qc + nq * h + h * 2 * f + f * h)
+    attn_fwd = 4 * w.d_h * attn_pairs(w) * w.a_t * w.micro_batch
+    return 3 * (gemm_fwd + attn_fwd), gemm_fwd, attn_fwd
+
+
+def kernel_work(w):
+    """Algorithmic work per launch: ('mfma', flops) or ('hbm', bytes)."""
+    out = {k: ("mfma", 2 * m * n * kk) for k, (m, n, kk) in gemm_shapes(w).items()}
+    _, _, attn_fwd = layer_flops(w)
+    out["attn_fwd"] = ("mfma", attn_fwd)
+    out["attn_bwd"] = ("mfma", 2 * attn_fwd)
+    rows = w.micro_batch * w.s_sp
+    out["rmsnorm_fwd"] = ("hbm", 2 * rows * w.hidden * 2 + 2 * w.hidden)
+    out["rmsnorm_bwd"] = ("hbm", 4 * rows * w.hidden * 2 + 2 * w.hidden)
+    return out
+
+
+def lm_flops(w):
+    return 3 * 2 * w.tokens * w.v_t * w.hidden
+
+
+# ------------------------------------------------------------------ runs
+
+def run_layer(w, steps, warmup, profile):
+    import torch
+    import paper_2411_06465_amd as L
+    import workloads as W
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+    wb, ab = W.layer_weights(w), W.layer_activations(w)
+    weights = {k: dev(v) for k, v in wb.items()}
+    x, dy = dev(ab["x"]), dev(ab["dy"])
+    peers = {k: dev(v) for k, v in ab["peers"].items()}
+    del wb, ab
+    y, dx = torch.empty_like(x), torch.empty_like(x)
+    grads = {k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in weights.items()}
+    d_rk = d_rv = None
+    if w.cp > 1:
+        shape = (w.micro_batch, w.seq - w.s_c, w.k_t * w.d_h)
+        d_rk = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+        d_rv = torch.empty_like(d_rk)
+    model, par = L.make_model(**w.model()), L.make_parallel(**w.parallel())
+    fws, bws = L.l4d_layer_workspace_bytes(model, par)
+    est = L.mem_estimate(model, par)
+    cap = est["act_bytes_per_layer"] + 4 * w.micro_batch * w.a_t * w.s_c + max(fws, bws) + (16 << 20)
+    arena = L.Arena.on(torch.empty(cap, dtype=torch.uint8, device="cuda"))
+
+    def step():
+        L.mem_estimate(model, par)
+        st = L.llama_layer_fwd(model, par, weights, x, y, arena, peers=peers)
+        L.llama_layer_bwd(model, par, weights, st, dy, dx, grads, arena, peers=peers, d_remote_k=d_rk,
+                          d_remote_v=d_rv)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    if profile:
+        L.l4d_profile_reset()
+        L.l4d_profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kernels = {}
+    if profile:
+        L.l4d_profile_enable(False)
+        kernels = L.l4d_profile_dump()
+    stash = est["act_bytes_per_layer"]
+    arena.destroy()
+    return (t1 - t0) / steps, kernels, stash
+
+
+def run_lm(w, steps, warmup):
+    import torch
+    import paper_2411_06465_amd as L
+    import workloads as W
+
+    inp = W.lm_head_inputs(w)
+    hid = torch.from_numpy(inp["hidden"].view(np.int16)).cuda().view(torch.bfloat16)
+    wl = torch.from_numpy(inp["w_lm"].view(np.int16)).cuda().view(torch.bfloat16)
+    tg = torch.from_numpy(inp["targets"]).cuda()
+    pl = torch.from_numpy(inp["peer_lse"]).cuda() if "peer_lse" in inp else None
+    pz = torch.from_numpy(inp["peer_target_logit"]).cuda() if "peer_target_logit" in inp else None
+    loss = torch.empty(w.tokens, dtype=torch.float32, device="cuda")
+    dh = torch.empty_like(hid)
+    dw = torch.zeros((w.v_t, w.hidden), dtype=torch.float32, device="cuda")
+    arena = L.Arena.on(torch.empty(L.l4d_lm_head_workspace_bytes(w.tokens, w.hidden, w.v_t) + (1 << 20),
+                                   dtype=torch.uint8, device="cuda"))
+
+    def step():
+        L.lm_head_xent(hid, wl, tg, loss, dh, dw, arena, vocab_start=w.tp_rank * w.v_t, peer_lse=pl,
+                       peer_target_logit=pz, grad_scale=1.0 / w.tokens)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps
+
+
+def cpu_baseline(w, seq):
+    """The oracle (float64 numpy, as written) on a bounded sample of the same
+    layer: same hidden/heads/FFN, sequence cut to `seq`."""
+    from threadpoolctl import threadpool_info
+    import workloads as W
+    from oracle import layer as OL
+    from oracle.bf16 import from_bits
+
+    ws = w.replace(name=w.name + "-cpu-sample", seq=seq)
+    wb, ab = W.layer_weights(ws), W.layer_activations(ws)
+    sh = OL.Shard(**ws.shard_kwargs())
+    wts = {k: from_bits(v) for k, v in wb.items()}
+    x, dy = from_bits(ab["x"]), from_bits(ab["dy"])
+    peers = {k: from_bits(v) for k, v in ab["peers"].items()}
+    t0 = time.perf_counter()
+    fw = OL.layer_forward(sh, wts, x, peers)
+    OL.layer_backward(sh, wts, fw, dy, peers)
+    dt = time.perf_counter() - t0
+    flops, _, _ = layer_flops(ws)
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{ws.name}: full layer fwd+bwd at seq {seq} (h {w.hidden}, {w.n_heads}/{w.n_kv_heads} heads, "
+                      f"FFN {w.ffn}), float64 numpy, {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-others", action="store_true")
+    ap.add_argument("--cpu-seq", type=int, default=1024)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU's shard: the library has no multi-GPU path; run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+
+    w = W.LLAMA2_7B
+    sec, kernels, stash = run_layer(w, args.steps, args.warmup, profile=True)
+    flops, gemm_fwd, attn_fwd = layer_flops(w)
+    value = flops / sec / 1e12
+
+    # roofline of the kernel with the largest share of the timed steps
+    work = kernel_work(w)
+    timed = {k: v for k, v in kernels.items() if k in work}
+    dom = max(timed, key=lambda k: timed[k][1])
+    launches, total_ms = timed[dom]
+    avg_s = total_ms / launches / 1e3
+    kind, amount = work[dom]
+    if kind == "mfma":
+        roof = {"bound": "mfma", "achieved": round(amount / avg_s / 1e12, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(amount / avg_s / 1e9, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = None
+    roof["kernel"] = dom
+    roof["avg_ms"] = round(total_ms / launches, 4)
+
+    kern = {}
+    for k, (n, ms) in sorted(kernels.items(), key=lambda kv: -kv[1][1]):
+        e = {"launches_per_step": n / args.steps, "ms_per_step": round(ms / args.steps, 4)}
+        if k in work:
+            kind_k, amt = work[k]
+            per_launch_s = ms / n / 1e3
+            if kind_k == "mfma":
+                e["tflops"] = round(amt / per_launch_s / 1e12, 1)
+            else:
+                e["gbs"] = round(amt / per_launch_s / 1e9, 1)
+        kern[k] = e
+
+    out = {
+        "metric": "TFLOP/s per GPU, Llama layer fwd+bwd shard; % of bf16 MFMA peak",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(sec * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "llama2-7b-shaped decoder layer, forward+backward shard: hidden 4096, 32 q / 32 kv "
+                               "heads (d_h 128), FFN 11008, seq 4096, micro-batch 1, TP1 CP1",
+                   "global_batch": 1, "seq_len": w.seq, "parallelism": "tp1-cp1 (one rank)",
+                   "model_flops_per_step": flops, "stash_bytes_per_layer": stash},
+        "pct_of_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "roofline": roof,
+        "kernels": kern,
+    }
+
+    if not args.no_others:
+        others = {}
+        for ow in (W.LLAMA3_8B_TP2CP2, W.LLAMA3_70B_TP8):
+            s2, _, _ = run_layer(ow, max(5, args.steps // 2), 2, profile=False)
+            f2, _, _ = layer_flops(ow)
+            others[ow.name] = {"tflops": round(f2 / s2 / 1e12, 2), "ms_per_step": round(s2 * 1e3, 3),
+                               "pct_of_bf16_peak": round(100 * f2 / s2 / 1e12 / PEAK_BF16_TFLOPS, 2)}
+            torch.cuda.empty_cache()
+        lw = W.LLAMA3_8B_LM_TP4
+        s3 = run_lm(lw, max(5, args.steps // 2), 2)
+        others[lw.name] = {"tflops": round(lm_flops(lw) / s3 / 1e12, 2), "ms_per_step": round(s3 * 1e3, 3),
+                           "pct_of_bf16_peak": round(100 * lm_flops(lw) / s3 / 1e12 / PEAK_BF16_TFLOPS, 2)}
+        out["other_workloads"] = others
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seq)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -188,7 +188,7 @@ def attention_bwd(sh, Q, K, V, q_pos, k_pos, dctx):
 
 def _tokens_t(a, b):
     """sum over batch and tokens of a^T b: [b, n, p], [b, n, q] -> [p, q]."""
-    return np.einsum("bnp,bnq->pq", a, b, optimize=True)
+    return a.reshape(-1, a.shape[-1]).T @ b.reshape(-1, b.shape[-1])
 
 
 # ---------------------------------------------------------------- the layer

@@ -458,7 +458,7 @@ struct FwdWs {
   uint64_t rope, o_send, ffn_send, total;
 };
 struct BwdWs {
-  uint64_t rope, dgu, dxn2, dh1, dctx, delta, dqkv, dxn1, partial, dxn2_send, dxn1_send, total;
+  uint64_t rope, dgu, dxn2, dh1, dctx, delta, dqkv, dxn1, partial, dxn2_send, dxn1_send, dkv, total;
 };
 
 FwdWs plan_fwd(const Shard& x, const l4d_peer_outputs* sends) {
@@ -488,6 +488,9 @@ BwdWs plan_bwd(const Shard& x, const l4d_peer_outputs* sends) {
   w.partial = cv.take((uint64_t)rmsnorm_bwd_partials(x.b * x.s_sp) * x.h * 4);
   w.dxn2_send = (x.t > 1 && !(sends && sends->dxn2_partial)) ? cv.take(peer_rows) : 0;
   w.dxn1_send = (x.t > 1 && !(sends && sends->dxn1_partial)) ? cv.take(peer_rows) : 0;
+  // fp32 dK/dV partials when the query heads of a kv-head are split (at most a/k slices)
+  const int64_t group = x.a / x.k;
+  w.dkv = group > 1 ? cv.take(2 * (uint64_t)group * x.b * x.s * x.k_t * x.d * 4) : 0;
   w.total = cv.used;
   return w;
 }
@@ -629,6 +632,7 @@ void key_segments(const Shard& x, AttnParams& ap, const uint16_t* K, const uint1
 
 AttnParams attn_params(const Shard& x) {
   AttnParams ap{};
+  ap.n_split = 1;
   ap.b = (int32_t)x.b;
   ap.a_t = (int32_t)x.a_t;
   ap.k_t = (int32_t)x.k_t;
@@ -856,6 +860,16 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
                  static_cast<const uint16_t*>(pi.remote_v), dqkv, static_cast<uint16_t*>(d_remote_k),
                  static_cast<uint16_t*>(d_remote_v), static_cast<const uint16_t*>(pi.cp_peer_dk),
                  static_cast<const uint16_t*>(pi.cp_peer_dv));
+    ap.total_keys = 0;
+    for (int i = 0; i < ap.n_seg; ++i) {
+      ap.seg_key0[i] = ap.total_keys;
+      ap.total_keys += ap.seg[i].n;
+    }
+    ap.n_split = attn_bwd_splits(ap);
+    if (ap.n_split > 1) {
+      ap.dkv_partial = reinterpret_cast<float*>(wsb + plan.dkv);
+      ap.partial_half = (int64_t)ap.n_split * x.b * ap.total_keys * x.k_t * x.d;
+    }
     if ((r = launch("attn_bwd", s, [&] { return attn_bwd(ap, s); }))) return r;
     // QKV projection
     if ((r = run_gemm("gemm_qkv_dx", s, tok, x.h, qc, op(RowSrc::plain(dqkv, qc), tok), Layout::KC,

@@ -7,19 +7,24 @@
 // rank's own context-parallel chunks and the remote chunks of the other CP
 // ranks.  A key is visible to a query iff key position <= query position.
 //
-// Layout choices (gfx950, wave64, v_mfma_f32_32x32x16_bf16):
-//  * scores are computed transposed, S^T = K Q^T, so that each lane owns one
-//    query column of the accumulator; row statistics are then per-lane
-//    scalars plus one cross-half exchange, and the bf16 probabilities already
-//    sit in the B-operand layout of the next product O^T += V^T P^T (the
-//    contraction index is permuted consistently on both operands).
-//  * V (and, in the backward, Q^T, dO^T, K^T) are transposed in registers on
-//    their way into LDS; K-like tiles are stored d-contiguous with an XOR
-//    swizzle of the 16-byte chunks, transposed tiles token-contiguous with an
-//    XOR swizzle of the 8-byte units.
-//  * dK/dV accumulate over all q-heads of a kv-head inside one workgroup, and
-//    dQ has its own kernel, so there are no atomics and results are
-//    deterministic.
+// gfx950 design:
+//  * every K/V/Q/dO tile is copied global -> LDS with global_load_lds_dwordx4
+//    (no staging registers) into a row-major tile with an XOR swizzle of its
+//    16-byte chunks; two separate LDS buffers alternate so that the next tile
+//    streams in while the current one is used;
+//  * operands that need the token index contiguous (V in P V, Q and dO in the
+//    dK/dV products, K in dQ) are read transposed straight from those tiles
+//    with ds_read_b64_tr_b16 (16 lanes x 4 rows -> 4 rows per lane);
+//  * scores are computed transposed where that puts one query per lane
+//    (forward, dQ), so the softmax statistics are per-lane scalars; the bf16
+//    probabilities then feed the next MFMA from registers with the
+//    contraction index permuted consistently on both operands;
+//  * masks are applied only on tiles that straddle the diagonal;
+//  * 256 threads and 64 KB of LDS per workgroup: two workgroups per CU.
+//  * dK/dV are accumulated over the query heads of a kv-head inside one
+//    workgroup, or, when that leaves too few workgroups, over a slice of them
+//    with an fp32 partial per slice that a small kernel sums: no atomics, the
+//    result is deterministic.
 #include <math.h>
 
 #include "kernels.h"
@@ -28,13 +33,18 @@ namespace l4d {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
+#define GPTR(p) ((const __attribute__((address_space(1))) void*)(p))
+#define LPTR(p) ((__attribute__((address_space(3))) void*)(p))
+
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr int KT = 64;            // keys per tile (forward, dQ)
+constexpr int QT = 32;            // queries per tile (dK/dV)
 
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
@@ -42,59 +52,68 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
 }
 __device__ __forceinline__ float lo16(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float hi16(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
+__device__ __forceinline__ void wait_tiles() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // ------------------------------------------------------------------ LDS tiles
-// R tile: [rows][D] bf16, 16-byte chunk c of row r at ((c ^ (r & 7)) << 4).
+// Row-major [rows][D] bf16 tile; 16-byte chunk c of row r sits at chunk c ^ swz(r).
 template <int D>
-__device__ __forceinline__ int r_off(int row, int chunk) {
-  return row * (D * 2) + ((chunk ^ (row & 7)) << 4);
+__device__ __forceinline__ int swz(int row) {
+  return D == 128 ? ((row & 7) << 1) : (row & 7);
 }
-// T tile: [D][64] bf16 (64 tokens per d-row), 8-byte unit u of row d at ((u ^ (d & 15)) << 3).
-__device__ __forceinline__ int t_off(int drow, int unit) { return drow * 128 + ((unit ^ (drow & 15)) << 3); }
+template <int D>
+__device__ __forceinline__ int t_off(int row, int chunk) {
+  return row * (D * 2) + ((chunk ^ swz<D>(row)) << 4);
+}
 
-// Write an 8 (tokens) x 8 (d) block, v[j] = token t0+j, d-chunk dc.
-template <int D>
-__device__ __forceinline__ void put_r(uint8_t* lds, int t0, int dc, const u32x4 (&v)[8]) {
+// Copy rows [0, ROWS) of src (row stride ld, rows >= n_valid clamped to the
+// last valid row) into an LDS tile; the four waves of the block share the work.
+template <int D, int ROWS>
+__device__ __forceinline__ void tile_load(uint8_t* lds, const uint16_t* src, int64_t ld, int n_valid, int wave,
+                                          int lane) {
+  constexpr int CH = D / 8;              // 16-byte chunks per row
+  constexpr int RPK = 64 / CH;           // rows per 1 KB wave chunk
+  constexpr int NKB = ROWS / RPK;
+  const int last = n_valid - 1;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) *reinterpret_cast<u32x4*>(lds + r_off<D>(t0 + j, dc)) = v[j];
-}
-__device__ __forceinline__ void put_t(uint8_t* lds, int t0, int dc, const u32x4 (&v)[8]) {
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int d = i >> 1;
-    uint32_t o[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint32_t a = v[2 * e][d], b = v[2 * e + 1][d];
-      o[e] = (i & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
-    }
-    const int drow = dc * 8 + i;
-    *reinterpret_cast<u32x2*>(lds + t_off(drow, t0 >> 2)) = u32x2{o[0], o[1]};
-    *reinterpret_cast<u32x2*>(lds + t_off(drow, (t0 >> 2) + 1)) = u32x2{o[2], o[3]};
+  for (int q = wave; q < NKB; q += 4) {
+    const int row = q * RPK + lane / CH;
+    const int lc = (lane % CH) ^ swz<D>(row);
+    const int r = row < last ? row : last;
+    __builtin_amdgcn_global_load_lds(GPTR(src + static_cast<int64_t>(r) * ld + lc * 8), LPTR(lds + q * 1024), 16, 0,
+                                     0);
   }
 }
 
-// A-operand fragment from an R tile: rows base + lane%32, d-chunk 2*kk + lane/32.
+// MFMA operand with the tile's rows as its 32 rows: rows row0 + lane%32,
+// contraction chunk 2*kk + lane/32 (d = 16 kk + 8 (lane/32) + 0..7).
 template <int D>
-__device__ __forceinline__ bf16x8 frag_r(const uint8_t* lds, int base, int kk, int lane) {
-  return *reinterpret_cast<const bf16x8*>(lds + r_off<D>(base + (lane & 31), 2 * kk + (lane >> 5)));
+__device__ __forceinline__ bf16x8 frag_rows(const uint8_t* lds, int row0, int kk, int lane) {
+  return *reinterpret_cast<const bf16x8*>(lds + t_off<D>(row0 + (lane & 31), 2 * kk + (lane >> 5)));
 }
-// A-operand fragment from a T tile: d-row drow0 + lane%32; the 16 contraction
-// slots of token group g16 (tokens 16*g16 .. +15) are ordered like the lanes'
-// accumulator rows of a 32x32 MFMA: slots 0-3 -> tokens 4*hh+0..3,
-// slots 4-7 -> tokens 8+4*hh+0..3, hh = lane/32.
-__device__ __forceinline__ bf16x8 frag_t(const uint8_t* lds, int drow0, int g16, int lane) {
-  const int drow = drow0 + (lane & 31);
-  const int u = g16 * 4 + (lane >> 5);
-  const u32x2 a = *reinterpret_cast<const u32x2*>(lds + t_off(drow, u));
-  const u32x2 b = *reinterpret_cast<const u32x2*>(lds + t_off(drow, u + 2));
-  return __builtin_bit_cast(bf16x8, u32x4{a[0], a[1], b[0], b[1]});
+// MFMA operand with the tile's columns as its rows: d = 32 dt + lane%32; its 8
+// contraction slots are tile rows 16 g16 + {4h .. 4h+3, 8+4h .. 8+4h+3},
+// h = lane/32 -- the same order in which a lane holds accumulator rows of a
+// 32x32 MFMA (see frag_acc).  Two transposing 64-bit LDS reads.
+template <int D>
+__device__ __forceinline__ bf16x8 frag_cols(const uint8_t* lds, int dt, int g16, int lane) {
+  const int li = lane & 15;
+  const int row = 16 * g16 + 4 * (lane >> 5) + (li >> 2);
+  const int d = 32 * dt + 16 * ((lane >> 4) & 1) + 4 * (li & 3);
+  const int off = t_off<D>(row, d >> 3) + ((d & 7) << 1);
+  const int off8 = t_off<D>(row + 8, d >> 3) + ((d & 7) << 1);
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      reinterpret_cast<__attribute__((address_space(3))) i16x4*>(LPTR(const_cast<uint8_t*>(lds) + off)));
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      reinterpret_cast<__attribute__((address_space(3))) i16x4*>(LPTR(const_cast<uint8_t*>(lds) + off8)));
+  return __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, a)[0], __builtin_bit_cast(u32x2, a)[1],
+                                          __builtin_bit_cast(u32x2, b)[0], __builtin_bit_cast(u32x2, b)[1]});
 }
-// B-operand fragment from 8 accumulator registers i0..i0+7 (probabilities).
+// Operand from 8 accumulator registers i0..i0+7 (rows 16 (i0/8) + {4h..4h+3, 8+4h..}).
 __device__ __forceinline__ bf16x8 frag_acc(const f32x16& s, int i0) {
   return __builtin_bit_cast(bf16x8, u32x4{pack2(s[i0], s[i0 + 1]), pack2(s[i0 + 2], s[i0 + 3]),
                                           pack2(s[i0 + 4], s[i0 + 5]), pack2(s[i0 + 6], s[i0 + 7])});
@@ -107,7 +126,7 @@ __device__ __forceinline__ int qpos(const ChunkMap& m, int row) {
   return m.chunk_id[c] * m.chunk_len + (row - c * m.chunk_len);
 }
 
-// Locate key tile `tile` (of `tsz` tokens) across the segments.
+// Key tile `tile` (of `tsz` tokens) across the segments.
 __device__ __forceinline__ bool find_tile(const AttnParams& p, int tile, int tsz, int& seg, int& t0) {
   int acc = 0;
   for (int s = 0; s < p.n_seg; ++s) {
@@ -126,23 +145,22 @@ __device__ __forceinline__ int total_tiles(const AttnParams& p, int tsz) {
   for (int s = 0; s < p.n_seg; ++s) acc += (p.seg[s].n + tsz - 1) / tsz;
   return acc;
 }
-
-// Load an 8-token x 8-d block of K or V (or Q / dO) from global; rows past n are zero.
-__device__ __forceinline__ void load8(const uint16_t* base, int64_t ld, int t0, int n, int dcol,
-                                      u32x4 (&v)[8]) {
-#pragma unroll
-  for (int j = 0; j < 8; ++j)
-    v[j] = (t0 + j < n) ? *reinterpret_cast<const u32x4*>(base + static_cast<int64_t>(t0 + j) * ld + dcol)
-                        : u32x4{0u, 0u, 0u, 0u};
+// Next key tile at or after `from` whose first key a query at pos_max can see.
+__device__ __forceinline__ int next_key_tile(const AttnParams& p, int from, int ntiles, int pos_max, int& seg,
+                                             int& t0) {
+  for (int t = from; t < ntiles; ++t) {
+    if (!find_tile(p, t, KT, seg, t0)) break;
+    if (p.seg[seg].pos0 + t0 <= pos_max) return t;
+  }
+  return ntiles;
 }
 
 // ------------------------------------------------------------------ forward
-// grid: (q tiles of 128, a_t heads, b); block 256 = 4 waves x 32 queries.
+// grid: (q tiles of 128, a_t heads, b); 4 waves x 32 queries.
 template <int D>
-__global__ void __launch_bounds__(256) attn_fwd_kernel(AttnParams p) {
-  constexpr int KT = 64;                        // keys per tile
-  constexpr int TILE = KT * D * 2;              // bytes of one K (R) or V^T (T) tile
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2][2][TILE];
+__global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
+  constexpr int TB = KT * D * 2;
+  __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n_qt = (p.n_q + 127) / 128;
   const int qt = n_qt - 1 - blockIdx.x;         // heaviest tiles first
@@ -154,121 +172,101 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(AttnParams p) {
   const int my_pos = q_ok ? qpos(p.qmap, my_q) : -1;
   const int blk_last = min(q_row0 + 127, p.n_q - 1);
   const int pos_min = qpos(p.qmap, q_row0), pos_max = qpos(p.qmap, blk_last);
+  const int rbase = 4 * (lane >> 5);
 
-  // Q fragments (B operand): query my_q, d-chunk 2kk + lane/32.
   bf16x8 qf[D / 16];
   {
-    const uint16_t* qb = p.q + bi * p.q_bstride + static_cast<int64_t>(my_q) * p.q_ld + hq * D;
+    const uint16_t* qb = p.q + bi * p.q_bstride + static_cast<int64_t>(q_ok ? my_q : 0) * p.q_ld + hq * D;
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk)
-      qf[kk] = q_ok ? *reinterpret_cast<const bf16x8*>(qb + (2 * kk + (lane >> 5)) * 8) : bf16x8{};
+    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qb + (2 * kk + (lane >> 5)) * 8);
   }
-
   const float c = p.scale * kLog2e;
   float m_run = -INFINITY, l_run = 0.f;
   f32x16 o[D / 32];
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) o[i] = f32x16{};
 
-  // The tiles this block must visit: visible to at least one of its queries.
   const int ntiles = total_tiles(p, KT);
-  auto visible = [&](int tile, int& seg, int& t0) {
-    if (!find_tile(p, tile, KT, seg, t0)) return false;
-    return p.seg[seg].pos0 + t0 <= pos_max;
-  };
-  auto next_visible = [&](int from, int& seg, int& t0) {
-    for (int t = from; t < ntiles; ++t)
-      if (visible(t, seg, t0)) return t;
-    return ntiles;
-  };
-
-  // Loader role: threads 0..127 move K blocks, 128..255 V blocks.
-  const bool is_k = tid < 128;
-  const int lt = tid & 127;
-  const int tb = lt / (D / 8), dc = lt % (D / 8);     // token block (of 8), d-chunk
-  const bool loader = tb < KT / 8;
-  u32x4 stage[8];
-  auto gload = [&](int seg, int t0) {
-    if (!loader) return;
+  auto issue = [&](int seg, int t0, uint8_t* kt, uint8_t* vt) {
     const KvSeg& s = p.seg[seg];
-    const uint16_t* base = (is_k ? s.k : s.v) + bi * s.bstride + hk * D;
-    load8(base + static_cast<int64_t>(t0) * s.ld, s.ld, tb * 8, s.n - t0, dc * 8, stage);
+    const int64_t off = bi * s.bstride + static_cast<int64_t>(t0) * s.ld + hk * D;
+    tile_load<D, KT>(kt, s.k + off, s.ld, s.n - t0, wave, lane);
+    tile_load<D, KT>(vt, s.v + off, s.ld, s.n - t0, wave, lane);
   };
-  auto lstore = [&](int buf) {
-    if (!loader) return;
-    if (is_k) put_r<D>(smem[buf][0], tb * 8, dc, stage);
-    else put_t(smem[buf][1], tb * 8, dc, stage);
-  };
-
-  int seg, t0;
-  int cur = next_visible(0, seg, t0);
-  if (cur < ntiles) {
-    gload(seg, t0);
-    lstore(0);
-  }
-  __syncthreads();
-  int buf = 0;
-  while (cur < ntiles) {
-    const int cseg = seg, ct0 = t0;
-    const int nxt = next_visible(cur + 1, seg, t0);
-    if (nxt < ntiles) gload(seg, t0);
-
-    const KvSeg& s = p.seg[cseg];
-    const int kpos0 = s.pos0 + ct0;
-    const int kvalid = min(KT, s.n - ct0);
-    const bool need_mask = (kpos0 + KT - 1 > pos_min) || (kvalid < KT);
-
-    // S^T for 64 keys x 32 queries: two 32-key accumulators.
+  auto compute = [&](int seg, int t0, const uint8_t* kt, const uint8_t* vt) {
+    const KvSeg& s = p.seg[seg];
+    const int kpos0 = s.pos0 + t0;
+    const int kvalid = min(KT, s.n - t0);
     f32x16 sc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) sc[t2] = mfma(frag_r<D>(smem[buf][0], t2 * 32, kk, lane), qf[kk], sc[t2]);
-
+      for (int t2 = 0; t2 < 2; ++t2) sc[t2] = mfma(frag_rows<D>(kt, t2 * 32, kk, lane), qf[kk], sc[t2]);
+    if (kpos0 + KT - 1 > pos_min || kvalid < KT) {       // tile straddles the diagonal (or is ragged)
+      const int lim = min(my_pos - kpos0, kvalid - 1);   // last visible key row for this query
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (t2 * 32 + 8 * (i >> 2) + rbase + (i & 3) > lim) sc[t2][i] = -INFINITY;
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float v = sc[t2][i] * c;
-        if (need_mask) {
-          const int kr = t2 * 32 + acc_row(i, lane);
-          if (kr >= kvalid || kpos0 + kr > my_pos) v = -INFINITY;
-        }
-        sc[t2][i] = v;
-        mx = fmaxf(mx, v);
-      }
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[t2][i]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
+    const float m_new = fmaxf(m_run, mx * c);
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
+    const float alpha = fast_exp2(m_run - m_use);
     float rs = 0.f;
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float pr = exp2f(sc[t2][i] - m_use);
+        const float pr = fast_exp2(fmaf(sc[t2][i], c, -m_use));
         sc[t2][i] = pr;
         rs += pr;
       }
     l_run = l_run * alpha + rs;
     m_run = m_new;
+    if (__ballot(alpha != 1.0f)) {
 #pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
-    // O^T[d][q] += V^T[d][keys] P^T[keys][q]
+      for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
+    }
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         const bf16x8 pf = frag_acc(sc[t2], 8 * g);
 #pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) o[dt] = mfma(frag_t(smem[buf][1], dt * 32, t2 * 2 + g, lane), pf, o[dt]);
+        for (int dt = 0; dt < D / 32; ++dt) o[dt] = mfma(frag_cols<D>(vt, dt, t2 * 2 + g, lane), pf, o[dt]);
       }
+  };
 
-    if (nxt < ntiles) lstore(buf ^ 1);
+  int seg, t0, nseg, nt0;
+  int cur = next_key_tile(p, 0, ntiles, pos_max, seg, t0);
+  if (cur < ntiles) issue(seg, t0, k0, v0);
+  wait_tiles();
+  __syncthreads();
+  while (cur < ntiles) {
+    int nxt = next_key_tile(p, cur + 1, ntiles, pos_max, nseg, nt0);
+    if (nxt < ntiles) issue(nseg, nt0, k1, v1);
+    compute(seg, t0, k0, v0);
+    wait_tiles();
     __syncthreads();
-    buf ^= 1;
     cur = nxt;
+    seg = nseg;
+    t0 = nt0;
+    if (cur >= ntiles) break;
+    nxt = next_key_tile(p, cur + 1, ntiles, pos_max, nseg, nt0);
+    if (nxt < ntiles) issue(nseg, nt0, k0, v0);
+    compute(seg, t0, k1, v1);
+    wait_tiles();
+    __syncthreads();
+    cur = nxt;
+    seg = nseg;
+    t0 = nt0;
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -279,14 +277,12 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(AttnParams p) {
   for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-      const int d = dt * 32 + 8 * jj + 4 * (lane >> 5);
-      const u32x2 w = {pack2(o[dt][4 * jj] * inv, o[dt][4 * jj + 1] * inv),
-                       pack2(o[dt][4 * jj + 2] * inv, o[dt][4 * jj + 3] * inv)};
-      *reinterpret_cast<u32x2*>(ob + d) = w;
+      const int d = dt * 32 + 8 * jj + rbase;
+      *reinterpret_cast<u32x2*>(ob + d) = u32x2{pack2(o[dt][4 * jj] * inv, o[dt][4 * jj + 1] * inv),
+                                                pack2(o[dt][4 * jj + 2] * inv, o[dt][4 * jj + 3] * inv)};
     }
   if (lane < 32)
-    p.lse[(static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + my_q] =
-        (m_run + log2f(l_tot)) * kLn2;
+    p.lse[(static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + my_q] = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
 }
 
 // ------------------------------------------------------------------ backward: delta
@@ -299,7 +295,7 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(AttnParams p) {
   const int64_t bi = row / p.n_q, q = row % p.n_q;
   const uint16_t* o = p.o + bi * p.q_bstride + q * p.q_ld;
   const uint16_t* d = p.dout + bi * p.q_bstride + q * p.q_ld;
-  constexpr int CPH = D / 8;                 // 16-byte chunks per head
+  constexpr int CPH = D / 8;
   const int nch = p.a_t * CPH;
   for (int c0 = 0; c0 < nch; c0 += 64) {
     const int c = c0 + lane;
@@ -312,44 +308,41 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(AttnParams p) {
     }
 #pragma unroll
     for (int off = CPH / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-    if (c < nch && (c % CPH) == 0) {
-      const int h = c / CPH;
-      p.delta[(bi * p.a_t + h) * p.n_q + q] = s;
-    }
+    if (c < nch && (c % CPH) == 0) p.delta[(bi * p.a_t + c / CPH) * p.n_q + q] = s;
   }
 }
 
 // ------------------------------------------------------------------ backward: dK, dV
-// grid: (key blocks of 128 over all segments, k_t kv-heads, b); 4 waves x 32 keys.
-// Loops over the a/k query heads of the kv-head and over 64-query tiles.
+// grid: (key blocks of 128 over all segments, k_t * n_split, b); 4 waves x 32 keys.
+// Workgroup (kb, hk, split) sums over query heads hk*g + [split*hpb, (split+1)*hpb).
 template <int D>
-__global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(AttnParams p) {
-  constexpr int QT = 64;
-  constexpr int TILE = QT * D * 2;
-  // [buf][Q, Q^T, dO, dO^T]
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2][4][TILE];
-  __shared__ float s_lse[2][QT], s_delta[2][QT];
+__global__ void __launch_bounds__(256, 1) attn_bwd_dkdv_kernel(AttnParams p) {
+  constexpr int TB = QT * D * 2;
+  __shared__ __attribute__((aligned(16))) uint8_t q0[TB], g0[TB], q1[TB], g1[TB];   // Q and dO tiles
+  __shared__ __attribute__((aligned(16))) float st0[2][QT], st1[2][QT];             // lse*log2e, delta
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int hk = blockIdx.y, bi = blockIdx.z;
   const int group = p.a_t / p.k_t;
+  const int hpb = group / p.n_split;
+  const int hk = blockIdx.y / p.n_split, split = blockIdx.y % p.n_split;
+  const int bi = blockIdx.z;
   int seg, k0;
   if (!find_tile(p, blockIdx.x, 128, seg, k0)) return;
   const KvSeg& S = p.seg[seg];
-  const int kbase = k0 + wave * 32;               // this wave's first key (in the segment)
-  const int my_key = kbase + (lane & 31);
+  const int my_key = k0 + wave * 32 + (lane & 31);
   const bool key_ok = my_key < S.n;
   const int my_kpos = S.pos0 + my_key;
+  const int wave_kpos0 = S.pos0 + k0 + wave * 32;
   const int blk_kpos0 = S.pos0 + k0;
+  const int rbase = 4 * (lane >> 5);
 
-  // K and V fragments (B operands), key my_key, d-chunk 2kk + lane/32.
   bf16x8 kf[D / 16], vf[D / 16];
   {
-    const int64_t off = bi * S.bstride + static_cast<int64_t>(my_key) * S.ld + hk * D;
+    const int64_t off = bi * S.bstride + static_cast<int64_t>(key_ok ? my_key : 0) * S.ld + hk * D;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       const int dcol = (2 * kk + (lane >> 5)) * 8;
-      kf[kk] = key_ok ? *reinterpret_cast<const bf16x8*>(S.k + off + dcol) : bf16x8{};
-      vf[kk] = key_ok ? *reinterpret_cast<const bf16x8*>(S.v + off + dcol) : bf16x8{};
+      kf[kk] = *reinterpret_cast<const bf16x8*>(S.k + off + dcol);
+      vf[kk] = *reinterpret_cast<const bf16x8*>(S.v + off + dcol);
     }
   }
   f32x16 dk[D / 32], dv[D / 32];
@@ -360,118 +353,122 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(AttnParams p) {
   }
   const float c = p.scale * kLog2e;
   const int n_qt = (p.n_q + QT - 1) / QT;
-  const int total = group * n_qt;
-  // a query tile matters if its last query can see the block's first key
-  auto wanted = [&](int it) {
-    const int qt = it % n_qt;
-    const int last = min(qt * QT + QT - 1, p.n_q - 1);
-    return qpos(p.qmap, last) >= blk_kpos0;
-  };
+  const int total = hpb * n_qt;
+  const int head0 = hk * group + split * hpb;
   auto next_wanted = [&](int from) {
-    for (int it = from; it < total; ++it)
-      if (wanted(it)) return it;
+    for (int it = from; it < total; ++it) {
+      const int qt = it % n_qt;
+      const int last = min(qt * QT + QT - 1, p.n_q - 1);
+      if (qpos(p.qmap, last) >= blk_kpos0) return it;
+    }
     return total;
   };
-  // loaders: threads 0..127 Q blocks, 128..255 dO blocks (64 tokens x D)
-  const bool is_q = tid < 128;
-  const int lt = tid & 127;
-  const int tb = lt / (D / 8), dc = lt % (D / 8);
-  const bool loader = tb < QT / 8;
-  u32x4 stage[8];
-  auto gload = [&](int it) {
-    const int hq = hk * group + it / n_qt, qt = it % n_qt;
-    if (loader) {
-      const uint16_t* base = (is_q ? p.q : p.dout) + bi * p.q_bstride + hq * D +
-                             static_cast<int64_t>(qt * QT) * p.q_ld;
-      load8(base, p.q_ld, tb * 8, p.n_q - qt * QT, dc * 8, stage);
-    }
-  };
-  auto lstore = [&](int buf, int it) {
-    const int hq = hk * group + it / n_qt, qt = it % n_qt;
-    if (loader) {
-      put_r<D>(smem[buf][is_q ? 0 : 2], tb * 8, dc, stage);
-      put_t(smem[buf][is_q ? 1 : 3], tb * 8, dc, stage);
-    }
-    if (tid < QT) {
+  auto issue = [&](int it, uint8_t* qt_l, uint8_t* gt_l, float (*st)[QT]) {
+    const int hq = head0 + it / n_qt, qt = it % n_qt;
+    if (tid < QT) {     // before the tile copies, so its wait does not cover them
       const int q = qt * QT + tid;
-      const int64_t idx = (static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + q;
-      s_lse[buf][tid] = q < p.n_q ? p.lse[idx] * kLog2e : INFINITY;
-      s_delta[buf][tid] = q < p.n_q ? p.delta[idx] : 0.f;
+      const int64_t idx = (static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + (q < p.n_q ? q : 0);
+      st[0][tid] = q < p.n_q ? p.lse[idx] * kLog2e : INFINITY;
+      st[1][tid] = q < p.n_q ? p.delta[idx] : 0.f;
+    }
+    const int64_t off = bi * p.q_bstride + static_cast<int64_t>(qt * QT) * p.q_ld + hq * D;
+    tile_load<D, QT>(qt_l, p.q + off, p.q_ld, p.n_q - qt * QT, wave, lane);
+    tile_load<D, QT>(gt_l, p.dout + off, p.q_ld, p.n_q - qt * QT, wave, lane);
+  };
+  auto compute = [&](int it, const uint8_t* qt_l, const uint8_t* gt_l, const float (*st)[QT]) {
+    const int qt = it % n_qt;
+    const int qr0 = qt * QT;
+    const int qlast = min(qr0 + QT - 1, p.n_q - 1);
+    const int qp0 = qpos(p.qmap, qr0), qpl = qpos(p.qmap, qlast);
+    if (qpl < wave_kpos0) return;                        // every query of the tile precedes this wave's keys
+    f32x16 sc = f32x16{}, dp = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      sc = mfma(frag_rows<D>(qt_l, 0, kk, lane), kf[kk], sc);
+      dp = mfma(frag_rows<D>(gt_l, 0, kk, lane), vf[kk], dp);
+    }
+    const bool full = qp0 >= wave_kpos0 + 31 && qlast == qr0 + QT - 1 && qpl - qp0 == QT - 1;
+    const bool contiguous = qpl - qp0 == qlast - qr0;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const float4 ls = *reinterpret_cast<const float4*>(&st[0][8 * jj + rbase]);
+      const float4 de = *reinterpret_cast<const float4*>(&st[1][8 * jj + rbase]);
+      const float lsv[4] = {ls.x, ls.y, ls.z, ls.w}, dev[4] = {de.x, de.y, de.z, de.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = 4 * jj + u;
+        float pr = fast_exp2(fmaf(sc[i], c, -lsv[u]));
+        if (!full) {
+          const int qr = 8 * jj + rbase + u;
+          const int qp = contiguous ? qp0 + qr : (qr0 + qr <= qlast ? qpos(p.qmap, qr0 + qr) : -1);
+          if (qr0 + qr > qlast || my_kpos > qp || !key_ok) pr = 0.f;
+        }
+        sc[i] = pr;
+        dp[i] = pr * (dp[i] - dev[u]);
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const bf16x8 pf = frag_acc(sc, 8 * g);
+      const bf16x8 sf = frag_acc(dp, 8 * g);
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) {
+        dv[dt] = mfma(frag_cols<D>(gt_l, dt, g, lane), pf, dv[dt]);
+        dk[dt] = mfma(frag_cols<D>(qt_l, dt, g, lane), sf, dk[dt]);
+      }
     }
   };
 
   int cur = next_wanted(0);
-  if (cur < total) {
-    gload(cur);
-    lstore(0, cur);
-  }
+  if (cur < total) issue(cur, q0, g0, st0);
+  wait_tiles();
   __syncthreads();
-  int buf = 0;
   while (cur < total) {
-    const int nxt = next_wanted(cur + 1);
-    if (nxt < total) gload(nxt);
-    const int qt = cur % n_qt;
-    const int qr0 = qt * QT;
-    const uint8_t* tq = smem[buf][0];
-    const uint8_t* tqt = smem[buf][1];
-    const uint8_t* tdo = smem[buf][2];
-    const uint8_t* tdot = smem[buf][3];
-
-    // S[q][key] and dP[q][key] for 64 queries (two 32-row halves) x 32 keys.
-    f32x16 sc[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk)
-#pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        sc[h2] = mfma(frag_r<D>(tq, h2 * 32, kk, lane), kf[kk], sc[h2]);
-        dp[h2] = mfma(frag_r<D>(tdo, h2 * 32, kk, lane), vf[kk], dp[h2]);
-      }
-    // P = exp(S*scale - lse), dS = P (dP - delta), masked where key > query.
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int qr = h2 * 32 + acc_row(i, lane);
-        const int q = qr0 + qr;
-        float pr = 0.f;
-        if (key_ok && q < p.n_q && my_kpos <= qpos(p.qmap, q)) pr = exp2f(sc[h2][i] * c - s_lse[buf][qr]);
-        sc[h2][i] = pr;
-        dp[h2][i] = pr * (dp[h2][i] - s_delta[buf][qr]);
-      }
-    // dV^T[d][key] += dO^T[d][q] P[q][key];  dK^T[d][key] += Q^T[d][q] dS[q][key]
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-      for (int g = 0; g < 2; ++g) {
-        const bf16x8 pf = frag_acc(sc[h2], 8 * g);
-        const bf16x8 sf = frag_acc(dp[h2], 8 * g);
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) {
-          dv[dt] = mfma(frag_t(tdot, dt * 32, h2 * 2 + g, lane), pf, dv[dt]);
-          dk[dt] = mfma(frag_t(tqt, dt * 32, h2 * 2 + g, lane), sf, dk[dt]);
-        }
-      }
-    if (nxt < total) lstore(buf ^ 1, nxt);
+    int nxt = next_wanted(cur + 1);
+    if (nxt < total) issue(nxt, q1, g1, st1);
+    compute(cur, q0, g0, st0);
+    wait_tiles();
     __syncthreads();
-    buf ^= 1;
+    cur = nxt;
+    if (cur >= total) break;
+    nxt = next_wanted(cur + 1);
+    if (nxt < total) issue(nxt, q0, g0, st0);
+    compute(cur, q1, g1, st1);
+    wait_tiles();
+    __syncthreads();
     cur = nxt;
   }
 
   if (!key_ok) return;
-  // Outputs: lane owns key my_key; register i of tile dt is d = 32 dt + acc_row(i).
+  // lane owns key my_key; register i of tile dt is d = 32 dt + acc_row(i)
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt) dk[dt] *= p.scale;
+  if (p.n_split > 1) {
+    // fp32 partial [split][b][key (over segments)][k_t][D], summed by attn_dkv_reduce
+    const int64_t key_index = static_cast<int64_t>(p.seg_key0[seg]) + my_key;
+    const int64_t row = ((static_cast<int64_t>(split) * p.b + bi) * p.total_keys + key_index) * p.k_t + hk;
+    float* pk = p.dkv_partial + row * D;
+    float* pv = p.dkv_partial + p.partial_half + row * D;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int d = dt * 32 + 8 * jj + rbase;
+        *reinterpret_cast<float4*>(pk + d) = make_float4(dk[dt][4 * jj], dk[dt][4 * jj + 1], dk[dt][4 * jj + 2],
+                                                         dk[dt][4 * jj + 3]);
+        *reinterpret_cast<float4*>(pv + d) = make_float4(dv[dt][4 * jj], dv[dt][4 * jj + 1], dv[dt][4 * jj + 2],
+                                                         dv[dt][4 * jj + 3]);
+      }
+    return;
+  }
   const int64_t off = bi * S.bstride + static_cast<int64_t>(my_key) * S.ld + hk * D;
   const int64_t doff = bi * S.d_bstride + static_cast<int64_t>(my_key) * S.d_ld + hk * D;
-  constexpr int HALF_T = D / 64;   // tiles between a RoPE pair (d, d + D/2)
-#pragma unroll
-  for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) dk[dt][i] *= p.scale;
   if (S.rk) {
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const int d = dt * 32 + 8 * jj + 4 * (lane >> 5);
+        const int d = dt * 32 + 8 * jj + rbase;
         const u32x2 rk = *reinterpret_cast<const u32x2*>(S.rk + off + d);
         const u32x2 rv = *reinterpret_cast<const u32x2*>(S.rv + off + d);
         dk[dt][4 * jj] += lo16(rk[0]);
@@ -485,13 +482,13 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(AttnParams p) {
       }
   }
   if (S.rope) {
+    constexpr int HALF_T = D / 64;
     const float2* tab = p.rope + static_cast<int64_t>(S.rope_row0 + my_key) * (D / 2);
 #pragma unroll
     for (int dt = 0; dt < HALF_T; ++dt)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int d = dt * 32 + acc_row(i, lane);
-        const float2 cs = tab[d];
+        const float2 cs = tab[dt * 32 + acc_row(i, lane)];
         const float a = dk[dt][i], b = dk[dt + HALF_T][i];
         dk[dt][i] = a * cs.x + b * cs.y;              // rotate by -angle
         dk[dt + HALF_T][i] = b * cs.x - a * cs.y;
@@ -501,7 +498,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(AttnParams p) {
   for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-      const int d = dt * 32 + 8 * jj + 4 * (lane >> 5);
+      const int d = dt * 32 + 8 * jj + rbase;
       *reinterpret_cast<u32x2*>(S.dk + doff + d) =
           u32x2{pack2(dk[dt][4 * jj], dk[dt][4 * jj + 1]), pack2(dk[dt][4 * jj + 2], dk[dt][4 * jj + 3])};
       *reinterpret_cast<u32x2*>(S.dv + doff + d) =
@@ -509,14 +506,54 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(AttnParams p) {
     }
 }
 
+// Sum the per-slice fp32 partials, add the receipts, apply the inverse RoPE to
+// local keys and store bf16.  One 64-thread block per (key, kv-head, b); thread
+// j handles the RoPE pair (j, j + D/2) of dK and of dV.
+template <int D>
+__global__ void __launch_bounds__(64) attn_dkv_reduce_kernel(AttnParams p) {
+  const int key_index = blockIdx.x, hk = blockIdx.y, bi = blockIdx.z;
+  const int j = threadIdx.x;
+  if (j >= D / 2) return;
+  int seg = 0;
+  while (seg + 1 < p.n_seg && key_index >= p.seg_key0[seg + 1]) ++seg;
+  const KvSeg& S = p.seg[seg];
+  const int key = key_index - p.seg_key0[seg];
+  float a = 0.f, b = 0.f, va = 0.f, vb = 0.f;
+  for (int sp = 0; sp < p.n_split; ++sp) {
+    const int64_t row = ((static_cast<int64_t>(sp) * p.b + bi) * p.total_keys + key_index) * p.k_t + hk;
+    const float* pk = p.dkv_partial + row * D;
+    const float* pv = p.dkv_partial + p.partial_half + row * D;
+    a += pk[j];
+    b += pk[j + D / 2];
+    va += pv[j];
+    vb += pv[j + D / 2];
+  }
+  const int64_t off = bi * S.bstride + static_cast<int64_t>(key) * S.ld + hk * D;
+  if (S.rk) {
+    a += __uint_as_float(static_cast<uint32_t>(S.rk[off + j]) << 16);
+    b += __uint_as_float(static_cast<uint32_t>(S.rk[off + j + D / 2]) << 16);
+    va += __uint_as_float(static_cast<uint32_t>(S.rv[off + j]) << 16);
+    vb += __uint_as_float(static_cast<uint32_t>(S.rv[off + j + D / 2]) << 16);
+  }
+  if (S.rope) {
+    const float2 cs = p.rope[static_cast<int64_t>(S.rope_row0 + key) * (D / 2) + j];
+    const float ra = a * cs.x + b * cs.y, rb = b * cs.x - a * cs.y;
+    a = ra;
+    b = rb;
+  }
+  const int64_t doff = bi * S.d_bstride + static_cast<int64_t>(key) * S.d_ld + hk * D;
+  S.dk[doff + j] = f2bf(a);
+  S.dk[doff + j + D / 2] = f2bf(b);
+  S.dv[doff + j] = f2bf(va);
+  S.dv[doff + j + D / 2] = f2bf(vb);
+}
+
 // ------------------------------------------------------------------ backward: dQ
 // grid: (q tiles of 128, a_t heads, b); 4 waves x 32 queries; loops over key tiles.
 template <int D>
-__global__ void __launch_bounds__(256) attn_bwd_dq_kernel(AttnParams p) {
-  constexpr int KT = 64;
-  constexpr int TILE = KT * D * 2;
-  // [buf][K, K^T, V]
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2][3][TILE];
+__global__ void __launch_bounds__(256, 1) attn_bwd_dq_kernel(AttnParams p) {
+  constexpr int TB = KT * D * 2;
+  __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n_qt = (p.n_q + 127) / 128;
   const int qt = n_qt - 1 - blockIdx.x;
@@ -527,101 +564,89 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(AttnParams p) {
   const bool q_ok = my_q < p.n_q;
   const int my_pos = q_ok ? qpos(p.qmap, my_q) : -1;
   const int blk_last = min(q_row0 + 127, p.n_q - 1);
-  const int pos_max = qpos(p.qmap, blk_last);
+  const int pos_min = qpos(p.qmap, q_row0), pos_max = qpos(p.qmap, blk_last);
+  const int rbase = 4 * (lane >> 5);
 
   bf16x8 qf[D / 16], dof[D / 16];
   {
-    const int64_t off = bi * p.q_bstride + static_cast<int64_t>(my_q) * p.q_ld + hq * D;
+    const int64_t off = bi * p.q_bstride + static_cast<int64_t>(q_ok ? my_q : 0) * p.q_ld + hq * D;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       const int dcol = (2 * kk + (lane >> 5)) * 8;
-      qf[kk] = q_ok ? *reinterpret_cast<const bf16x8*>(p.q + off + dcol) : bf16x8{};
-      dof[kk] = q_ok ? *reinterpret_cast<const bf16x8*>(p.dout + off + dcol) : bf16x8{};
+      qf[kk] = *reinterpret_cast<const bf16x8*>(p.q + off + dcol);
+      dof[kk] = *reinterpret_cast<const bf16x8*>(p.dout + off + dcol);
     }
   }
   const int64_t sidx = (static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + (q_ok ? my_q : 0);
-  const float my_lse = q_ok ? p.lse[sidx] * kLog2e : INFINITY;
-  const float my_delta = q_ok ? p.delta[sidx] : 0.f;
+  const float my_lse = p.lse[sidx] * kLog2e;
+  const float my_delta = p.delta[sidx];
   const float c = p.scale * kLog2e;
   f32x16 dq[D / 32];
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) dq[i] = f32x16{};
 
   const int ntiles = total_tiles(p, KT);
-  auto next_visible = [&](int from, int& seg, int& t0) {
-    for (int t = from; t < ntiles; ++t) {
-      if (!find_tile(p, t, KT, seg, t0)) break;
-      if (p.seg[seg].pos0 + t0 <= pos_max) return t;
-    }
-    return ntiles;
-  };
-  const bool is_k = tid < 128;
-  const int lt = tid & 127;
-  const int tb = lt / (D / 8), dc = lt % (D / 8);
-  const bool loader = tb < KT / 8;
-  u32x4 stage[8];
-  auto gload = [&](int seg, int t0) {
-    if (!loader) return;
+  auto issue = [&](int seg, int t0, uint8_t* kt, uint8_t* vt) {
     const KvSeg& s = p.seg[seg];
-    const uint16_t* base = (is_k ? s.k : s.v) + bi * s.bstride + hk * D;
-    load8(base + static_cast<int64_t>(t0) * s.ld, s.ld, tb * 8, s.n - t0, dc * 8, stage);
+    const int64_t off = bi * s.bstride + static_cast<int64_t>(t0) * s.ld + hk * D;
+    tile_load<D, KT>(kt, s.k + off, s.ld, s.n - t0, wave, lane);
+    tile_load<D, KT>(vt, s.v + off, s.ld, s.n - t0, wave, lane);
   };
-  auto lstore = [&](int buf) {
-    if (!loader) return;
-    if (is_k) {
-      put_r<D>(smem[buf][0], tb * 8, dc, stage);
-      put_t(smem[buf][1], tb * 8, dc, stage);
-    } else {
-      put_r<D>(smem[buf][2], tb * 8, dc, stage);
-    }
-  };
-
-  int seg, t0;
-  int cur = next_visible(0, seg, t0);
-  if (cur < ntiles) {
-    gload(seg, t0);
-    lstore(0);
-  }
-  __syncthreads();
-  int buf = 0;
-  while (cur < ntiles) {
-    const int cseg = seg, ct0 = t0;
-    const int nxt = next_visible(cur + 1, seg, t0);
-    if (nxt < ntiles) gload(seg, t0);
-    const KvSeg& s = p.seg[cseg];
-    const int kpos0 = s.pos0 + ct0;
-    const int kvalid = min(KT, s.n - ct0);
-
+  auto compute = [&](int seg, int t0, const uint8_t* kt, const uint8_t* vt) {
+    const KvSeg& s = p.seg[seg];
+    const int kpos0 = s.pos0 + t0;
+    const int kvalid = min(KT, s.n - t0);
     f32x16 sc[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
       for (int t2 = 0; t2 < 2; ++t2) {
-        sc[t2] = mfma(frag_r<D>(smem[buf][0], t2 * 32, kk, lane), qf[kk], sc[t2]);
-        dp[t2] = mfma(frag_r<D>(smem[buf][2], t2 * 32, kk, lane), dof[kk], dp[t2]);
+        sc[t2] = mfma(frag_rows<D>(kt, t2 * 32, kk, lane), qf[kk], sc[t2]);
+        dp[t2] = mfma(frag_rows<D>(vt, t2 * 32, kk, lane), dof[kk], dp[t2]);
       }
+    const bool masked = kpos0 + KT - 1 > pos_min || kvalid < KT;
+    const int lim = q_ok ? min(my_pos - kpos0, kvalid - 1) : -1;
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int kr = t2 * 32 + acc_row(i, lane);
-        float pr = 0.f;
-        if (q_ok && kr < kvalid && kpos0 + kr <= my_pos) pr = exp2f(sc[t2][i] * c - my_lse);
-        sc[t2][i] = pr * (dp[t2][i] - my_delta);       // dS^T
+        float pr = fast_exp2(fmaf(sc[t2][i], c, -my_lse));
+        if (masked && t2 * 32 + 8 * (i >> 2) + rbase + (i & 3) > lim) pr = 0.f;
+        sc[t2][i] = pr * (dp[t2][i] - my_delta);            // dS^T
       }
-    // dQ^T[d][q] += K^T[d][keys] dS^T[keys][q]
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         const bf16x8 sf = frag_acc(sc[t2], 8 * g);
 #pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) dq[dt] = mfma(frag_t(smem[buf][1], dt * 32, t2 * 2 + g, lane), sf, dq[dt]);
+        for (int dt = 0; dt < D / 32; ++dt) dq[dt] = mfma(frag_cols<D>(kt, dt, t2 * 2 + g, lane), sf, dq[dt]);
       }
-    if (nxt < ntiles) lstore(buf ^ 1);
+  };
+
+  int seg, t0, nseg, nt0;
+  int cur = next_key_tile(p, 0, ntiles, pos_max, seg, t0);
+  if (cur < ntiles) issue(seg, t0, k0, v0);
+  wait_tiles();
+  __syncthreads();
+  while (cur < ntiles) {
+    int nxt = next_key_tile(p, cur + 1, ntiles, pos_max, nseg, nt0);
+    if (nxt < ntiles) issue(nseg, nt0, k1, v1);
+    compute(seg, t0, k0, v0);
+    wait_tiles();
     __syncthreads();
-    buf ^= 1;
     cur = nxt;
+    seg = nseg;
+    t0 = nt0;
+    if (cur >= ntiles) break;
+    nxt = next_key_tile(p, cur + 1, ntiles, pos_max, nseg, nt0);
+    if (nxt < ntiles) issue(nseg, nt0, k0, v0);
+    compute(seg, t0, k1, v1);
+    wait_tiles();
+    __syncthreads();
+    cur = nxt;
+    seg = nseg;
+    t0 = nt0;
   }
   if (!q_ok) return;
   constexpr int HALF_T = D / 64;
@@ -630,28 +655,20 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(AttnParams p) {
   for (int dt = 0; dt < HALF_T; ++dt)
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int d = dt * 32 + acc_row(i, lane);
-      const float2 cs = tab[d];
+      const float2 cs = tab[dt * 32 + acc_row(i, lane)];
       const float a = dq[dt][i] * p.scale, b = dq[dt + HALF_T][i] * p.scale;
       dq[dt][i] = a * cs.x + b * cs.y;
       dq[dt + HALF_T][i] = b * cs.x - a * cs.y;
     }
-  uint16_t* out = p.dq + bi * static_cast<int64_t>(p.n_q) * p.dq_ld + static_cast<int64_t>(my_q) * p.dq_ld + hq * D;
+  uint16_t* out = p.dq + (bi * static_cast<int64_t>(p.n_q) + my_q) * p.dq_ld + hq * D;
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-      const int d = dt * 32 + 8 * jj + 4 * (lane >> 5);
+      const int d = dt * 32 + 8 * jj + rbase;
       *reinterpret_cast<u32x2*>(out + d) =
           u32x2{pack2(dq[dt][4 * jj], dq[dt][4 * jj + 1]), pack2(dq[dt][4 * jj + 2], dq[dt][4 * jj + 3])};
     }
-}
-
-template <int D>
-hipError_t fwd_impl(const AttnParams& p, hipStream_t stream) {
-  const dim3 grid((p.n_q + 127) / 128, p.a_t, p.b);
-  hipLaunchKernelGGL(attn_fwd_kernel<D>, grid, dim3(256), 0, stream, p);
-  return hipGetLastError();
 }
 
 int count_blocks(const AttnParams& p, int tsz) {
@@ -661,19 +678,39 @@ int count_blocks(const AttnParams& p, int tsz) {
 }
 
 template <int D>
+hipError_t fwd_impl(const AttnParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3((p.n_q + 127) / 128, p.a_t, p.b), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+template <int D>
 hipError_t bwd_impl(const AttnParams& p, hipStream_t stream) {
   const int64_t rows = static_cast<int64_t>(p.b) * p.n_q;
   hipLaunchKernelGGL(attn_delta_kernel<D>, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(count_blocks(p, 128), p.k_t, p.b), dim3(256), 0, stream, p);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(count_blocks(p, 128), p.k_t * p.n_split, p.b), dim3(256), 0,
+                     stream, p);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (p.n_split > 1) {
+    hipLaunchKernelGGL(attn_dkv_reduce_kernel<D>, dim3(p.total_keys, p.k_t, p.b), dim3(64), 0, stream, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3((p.n_q + 127) / 128, p.a_t, p.b), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 
 }  // namespace
+
+int attn_bwd_splits(const AttnParams& p) {
+  // Split the query heads of a kv-head over workgroups until the dK/dV grid
+  // has at least 512 workgroups (two per CU) or every head has its own.
+  const int group = p.a_t / p.k_t;
+  const int base = count_blocks(p, 128) * p.k_t * p.b;
+  int n = 1;
+  while (base * n < 512 && n < group && group % (2 * n) == 0) n *= 2;
+  return n;
+}
 
 hipError_t attn_fwd(const AttnParams& p, hipStream_t stream) {
   if (p.n_q <= 0) return hipSuccess;

@@ -150,8 +150,17 @@ struct AttnParams {
   uint16_t* dq;                // [b][n_q][dq_ld] at column h*d_h, inverse RoPE applied
   int64_t dq_ld;
   const float2* rope;          // table used by the inverse RoPE
+  // dK/dV split over query-head slices (n_split > 1): fp32 partials
+  // [n_split][b][total_keys][k_t][d_h] for dK, then the same for dV at +partial_half
+  int32_t n_split;
+  int32_t total_keys;          // keys over all segments
+  int32_t seg_key0[kMaxSeg];   // index of each segment's first key among them
+  float* dkv_partial;
+  int64_t partial_half;
 };
 
+// Number of query-head slices the dK/dV pass uses for this shape (1 = none).
+int attn_bwd_splits(const AttnParams& p);
 hipError_t attn_fwd(const AttnParams& p, hipStream_t stream);
 hipError_t attn_bwd(const AttnParams& p, hipStream_t stream);
 
