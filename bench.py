@@ -67,7 +67,8 @@ def kernel_work(w):
     out = {k: ("mfma", 2 * m * n * kk) for k, (m, n, kk) in gemm_shapes(w).items()}
     _, _, attn_fwd = layer_flops(w)
     out["attn_fwd"] = ("mfma", attn_fwd)
-    out["attn_bwd"] = ("mfma", 2 * attn_fwd)
+    out["attn_bwd_dkdv"] = ("mfma", attn_fwd)          # dK, dV: half of the 2x-forward backward
+    out["attn_bwd_dq"] = ("mfma", attn_fwd)            # dQ: the other half
     rows = w.micro_batch * w.s_sp
     out["rmsnorm_fwd"] = ("hbm", 2 * rows * w.hidden * 2 + 2 * w.hidden)
     out["rmsnorm_bwd"] = ("hbm", 4 * rows * w.hidden * 2 + 2 * w.hidden)

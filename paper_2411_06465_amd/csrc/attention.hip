@@ -684,19 +684,19 @@ hipError_t fwd_impl(const AttnParams& p, hipStream_t stream) {
 }
 
 template <int D>
-hipError_t bwd_impl(const AttnParams& p, hipStream_t stream) {
-  const int64_t rows = static_cast<int64_t>(p.b) * p.n_q;
-  hipLaunchKernelGGL(attn_delta_kernel<D>, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(count_blocks(p, 128), p.k_t * p.n_split, p.b), dim3(256), 0,
-                     stream, p);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (p.n_split > 1) {
+hipError_t bwd_impl(const AttnParams& p, int part, hipStream_t stream) {
+  if (part == 0) {
+    const int64_t rows = static_cast<int64_t>(p.b) * p.n_q;
+    hipLaunchKernelGGL(attn_delta_kernel<D>, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, p);
+  } else if (part == 1) {
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(count_blocks(p, 128), p.k_t * p.n_split, p.b), dim3(256), 0,
+                       stream, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.n_split == 1) return e;
     hipLaunchKernelGGL(attn_dkv_reduce_kernel<D>, dim3(p.total_keys, p.k_t, p.b), dim3(64), 0, stream, p);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+  } else {
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3((p.n_q + 127) / 128, p.a_t, p.b), dim3(256), 0, stream, p);
   }
-  hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3((p.n_q + 127) / 128, p.a_t, p.b), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -719,10 +719,10 @@ hipError_t attn_fwd(const AttnParams& p, hipStream_t stream) {
   return hipErrorInvalidValue;
 }
 
-hipError_t attn_bwd(const AttnParams& p, hipStream_t stream) {
+hipError_t attn_bwd(const AttnParams& p, int part, hipStream_t stream) {
   if (p.n_q <= 0) return hipSuccess;
-  if (p.d_h == 128) return bwd_impl<128>(p, stream);
-  if (p.d_h == 64) return bwd_impl<64>(p, stream);
+  if (p.d_h == 128) return bwd_impl<128>(p, part, stream);
+  if (p.d_h == 64) return bwd_impl<64>(p, part, stream);
   return hipErrorInvalidValue;
 }
 

@@ -1,43 +1,48 @@
 // bf16 GEMM on the gfx950 matrix cores: C[m][n] = sum_k A(m,k) B(n,k), fp32
 // accumulation, with the layer's fused epilogues.
 //
-// Tiling: one 512-thread workgroup (8 waves, 2 per SIMD) owns a 256x256 tile
-// of C and walks K in steps of 64.  Both operand tiles (256 x 64 bf16 each)
-// are double-buffered in LDS (128 KB); each wave computes a 128 x 64 block as
-// 4 x 2 v_mfma_f32_32x32x16_bf16 accumulators.  Tiles are stored k-contiguous
-// in LDS with an XOR swizzle of the 16-byte chunks so that 8 consecutive rows
-// read by one MFMA fragment load hit distinct banks.  Operands whose
-// reduction index is not contiguous in memory (the weight operand of dX, both
-// operands of dW) are loaded as 8x8 blocks and transposed in registers on
-// their way to LDS, so every fragment read is one 16-byte LDS load.
+// Tiling: a 512-thread workgroup (8 waves, two per SIMD) owns a 256x256 tile
+// of C; each wave accumulates a 128x64 block as 4 x 2 tiles of
+// v_mfma_f32_32x32x16_bf16 (128 accumulator registers).  K advances in steps
+// of 32 through a 4-stage pipeline: operand tiles are copied global -> LDS by
+// global_load_lds_dwordx4 (one contiguous KB per wave instruction, no staging
+// registers) three steps ahead of their use.  Every stage buffer is its own
+// LDS object so the compiler knows a read of one stage cannot depend on the
+// copies still landing in the others.
 //
-// The two 32-column accumulator blocks of a wave sit PAIR columns apart, so
-// that one lane owns both members of a RoPE pair (i, i + d_h/2) or of a
-// gate/up pair; the epilogue stages each wave's fp32 block through LDS and
-// writes 8-column vectors.
+// Operand layouts: "KC" (reduction index contiguous: activations in the
+// forward, the output gradient in dX) is stored as two 16-k sub-blocks of
+// 256 rows x 32 bytes, the two halves of a row swapped on rows with bit 2
+// set: the 8 rows one fragment read touches fall in 8 different bank groups
+// and every fragment address is a per-lane base plus an immediate.  "MN"
+// (reduction index strided: the weight in dX, both operands of dW) is stored
+// as 32 k-rows x 256 columns with the 16-byte chunks XOR-swizzled by row, and
+// read with two ds_read_b64_tr_b16 that hand each lane 4 consecutive k of one
+// column -- the transpose happens in the LDS read, not in registers.
+//
+// A wave's two 32-column blocks sit PAIR columns apart, so the columns n and
+// n + PAIR land in the same lane and register: a RoPE pair (i, i + d_h/2) or a
+// gate/up pair of the fused FFN weight.  The epilogue stages 64 rows at a time
+// through LDS and hands 8-column vectors to the fused operation.
 #include "kernels.h"
 
 namespace l4d {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int BM = 256, BN = 256, BK = 64, NT = 512;
-constexpr int TILE_BYTES = 256 * BK * 2;            // one operand tile
-constexpr int STAGE_LD = 68;                        // fp32 words per staged row
-constexpr int STAGE_WAVE = 64 * STAGE_LD;           // fp32 words per wave
-constexpr int LDS_BYTES = 8 * STAGE_WAVE * 4;       // 139264 >= 4 * TILE_BYTES
-static_assert(LDS_BYTES >= 4 * TILE_BYTES, "LDS too small for the double buffer");
+#define GPTR(p) ((const __attribute__((address_space(1))) void*)(p))
+#define LPTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+constexpr int BM = 256, BN = 256, BK = 32, NT = 512;
+constexpr int TILE_BYTES = 256 * BK * 2;     // 16 KB per operand per stage
 constexpr int GROUP_M = 8;
 
-__device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * 128 + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 4);
-}
-
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
-__device__ __forceinline__ float bf2f(uint32_t u16) { return __uint_as_float(u16 << 16); }
 
 __device__ __forceinline__ u32x4 pack8(const float* v) {
   u32x4 r;
@@ -53,72 +58,90 @@ __device__ __forceinline__ void unpack8(u32x4 u, float* v) {
   }
 }
 
-// Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
-// contiguous range of tiles so that neighbouring tiles share its L2.
 __device__ __forceinline__ int xcd_remap(int bid, int nwg) {
-  const int X = 8;
+  const int X = 8;   // workgroups go round-robin over the 8 XCDs; give each a contiguous tile range
   int per = nwg / X, rem = nwg % X, xcd = bid % X, local = bid / X;
   return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
-// -------------------------------------------------------------- operand movement
-// Thread `tid` (0..255 of the half that loads this operand) moves one 8x8 block.
+// ------------------------------------------------------------------ LDS layouts
+// KC tile: 16-byte chunk c (0..3) of row r (0..255) in sub-block c/2.
+__device__ __forceinline__ int kc_off(int row, int chunk) {
+  return (chunk >> 1) * 8192 + row * 32 + (((chunk & 1) ^ ((row >> 2) & 1)) << 4);
+}
+// MN tile: k-row r (0..31), 16-byte chunk c (0..31) of its 256 columns.
+__device__ __forceinline__ int mn_swz(int row) { return (row & 3) << 1; }
+__device__ __forceinline__ int mn_off(int row, int chunk) { return row * 512 + ((chunk ^ mn_swz(row)) << 4); }
 
-template <Layout L>
-__device__ __forceinline__ void load_block(const Operand& op, int x0, int tile_idx, int k0, int K,
-                                           int tid, u32x4 (&v)[8]) {
-  const u32x4 zero = {0u, 0u, 0u, 0u};
-  if constexpr (L == Layout::KC) {
-    const int rb = tid >> 3, kb = tid & 7;
-    const int k = k0 + kb * 8;
-    const bool kok = k < K;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int xr = rb * 8 + j;
-      int64_t gx;
-      bool ok;
-      if (op.split_rows) {
-        const int i = tile_idx * 128 + (xr & 127);
-        ok = i < op.split_rows;
-        gx = (xr >= 128 ? op.split_off : 0) + i;
-      } else {
-        gx = x0 + xr;
-        ok = gx < op.rows;
-      }
-      v[j] = (ok && kok) ? *reinterpret_cast<const u32x4*>(op.src.row(gx) + k) : zero;
-    }
+// Each wave copies LDS KB number kb = wave and wave + 8 of both operand tiles.
+// KC: KB kb holds sub-block kb/8, rows 32*(kb%8) + lane/2 -- the same tile row
+// for both of a lane's copies, fixed over K.  Its source row is kept as a
+// 32-bit element offset, bit 31 selecting the peer base of a
+// sequence-parallel gather.
+__device__ __forceinline__ uint32_t kc_row(const Operand& op, int x0, int tile_idx, int wave, int lane) {
+  const int xr = 32 * wave + (lane >> 1);
+  int64_t gx;
+  if (op.split_rows) {
+    int i = tile_idx * 128 + (xr & 127);
+    if (i >= op.split_rows) i = op.split_rows - 1;
+    gx = (xr >= 128 ? op.split_off : 0) + i;
   } else {
-    const int rb = tid & 31, kb = tid >> 5;
-    const int x = x0 + rb * 8;
-    const bool xok = x < op.rows;
+    gx = x0 + xr;
+    if (gx >= op.rows) gx = op.rows - 1;
+  }
+  return op.src.row_index(gx);
+}
+
+__device__ __forceinline__ void copy_kc(uint8_t* lds, const Operand& op, uint32_t row_off, int k0, int K, int wave,
+                                        int lane) {
+  const int row = 32 * wave + (lane >> 1);
+  const uint16_t* base = ((row_off & 0x80000000u) ? op.src.peer : op.src.own) +
+                         static_cast<int64_t>(row_off & 0x7fffffffu) * op.src.ld;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int k = k0 + kb * 8 + j;
-      v[j] = (xok && k < K) ? *reinterpret_cast<const u32x4*>(op.src.row(k) + x) : zero;
-    }
+  for (int kk = 0; kk < 2; ++kk) {
+    const int hh = (lane & 1) ^ ((row >> 2) & 1);
+    int k = k0 + kk * 16 + hh * 8;
+    if (k >= K) k = K - 8;            // those fragments are zeroed before use
+    __builtin_amdgcn_global_load_lds(GPTR(base + k), LPTR(lds + (wave + 8 * kk) * 1024), 16, 0, 0);
   }
 }
 
+// MN: KB kb holds k-rows 2 kb + lane/32.
+__device__ __forceinline__ void copy_mn(uint8_t* lds, const Operand& op, int x0, int k0, int K, int wave,
+                                        int lane) {
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int kb = wave + 8 * q;
+    const int kr = 2 * kb + (lane >> 5);
+    const int lc = (lane & 31) ^ mn_swz(kr);
+    int k = k0 + kr;
+    if (k >= K) k = K - 1;
+    int x = x0 + lc * 8;
+    if (x >= op.rows) x = op.rows - 8;
+    const uint32_t o = op.src.row_index(k);
+    const uint16_t* base = (o & 0x80000000u) ? op.src.peer : op.src.own;
+    __builtin_amdgcn_global_load_lds(GPTR(base + static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld + x),
+                                     LPTR(lds + kb * 1024), 16, 0, 0);
+  }
+}
+
+// MFMA operand for rows x0 + lane%32 (x0 a multiple of 32), k = 16 kk + 8 (lane/32) + 0..7.
 template <Layout L>
-__device__ __forceinline__ void store_block(uint8_t* lds, int tid, const u32x4 (&v)[8]) {
+__device__ __forceinline__ bf16x8 frag(const uint8_t* lds, int x0, int kk, int lane) {
   if constexpr (L == Layout::KC) {
-    const int rb = tid >> 3, kb = tid & 7;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) *reinterpret_cast<u32x4*>(lds + lds_off(rb * 8 + j, kb)) = v[j];
+    return *reinterpret_cast<const bf16x8*>(lds + kc_off(x0 + (lane & 31), 2 * kk + (lane >> 5)));
   } else {
-    // v[j] holds k-row j of the block (8 consecutive x); emit x-row i (8 consecutive k).
-    const int rb = tid & 31, kb = tid >> 5;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int d = i >> 1;
-      u32x4 o;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t a = v[2 * e][d], b = v[2 * e + 1][d];
-        o[e] = (i & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
-      }
-      *reinterpret_cast<u32x4*>(lds + lds_off(rb * 8 + i, kb)) = o;
-    }
+    const int li = lane & 15;
+    const int row = 16 * kk + 8 * (lane >> 5) + (li >> 2);
+    const int x = x0 + 16 * ((lane >> 4) & 1) + 4 * (li & 3);
+    const int off = mn_off(row, x >> 3) + ((x & 7) << 1);
+    const int off4 = mn_off(row + 4, x >> 3) + ((x & 7) << 1);
+    const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        reinterpret_cast<__attribute__((address_space(3))) i16x4*>(LPTR(const_cast<uint8_t*>(lds) + off)));
+    const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        reinterpret_cast<__attribute__((address_space(3))) i16x4*>(LPTR(const_cast<uint8_t*>(lds) + off4)));
+    const u32x2 ua = __builtin_bit_cast(u32x2, a), ub = __builtin_bit_cast(u32x2, b);
+    return __builtin_bit_cast(bf16x8, u32x4{ua[0], ua[1], ub[0], ub[1]});
   }
 }
 
@@ -127,13 +150,12 @@ __device__ __forceinline__ void store_block(uint8_t* lds, int tid, const u32x4 (
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
 // lo: 8 columns starting at tile column `col`; hi: the 8 columns PAIR further.
-template <int PAIR>
-__device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn, int col,
-                                         float* lo, float* hi) {
+template <EpiKind KIND, int PAIR>
+__device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn, int col, float* lo, float* hi) {
   const EpiParams& e = p.epi;
   if (m >= p.M) return;
   const int n_lo = tn * BN + col;
-  switch (e.kind) {
+  switch (KIND) {
     case EpiKind::StoreBF16: {
       uint16_t* c = static_cast<uint16_t*>(e.c) + m * e.ldc;
       if (n_lo < p.N) *reinterpret_cast<u32x4*>(c + n_lo) = pack8(lo);
@@ -265,11 +287,26 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn,
   }
 }
 
+// Tile column of a wave's low 32-column block (wn = 0..3); its partner is PAIR further.
+template <int PAIR>
+__device__ __forceinline__ int lo_col(int wn) {
+  constexpr int PW = PAIR / 32;
+  return (wn / PW) * (2 * PAIR) + (wn % PW) * 32;
+}
+
 // -------------------------------------------------------------- the kernel
 
-template <Layout LA, Layout LB, int PAIR>
-__global__ void __launch_bounds__(NT) gemm_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+}
+
+template <Layout LA, Layout LB, EpiKind KIND, int PAIR>
+__global__ void __launch_bounds__(NT, 1) gemm_kernel(GemmParams p) {  // 8 waves: 2 per SIMD
+  __shared__ __attribute__((aligned(16))) uint8_t a0[TILE_BYTES], b0[TILE_BYTES], a1[TILE_BYTES], b1[TILE_BYTES];
+  __shared__ __attribute__((aligned(16))) uint8_t a2[TILE_BYTES], b2[TILE_BYTES], a3[TILE_BYTES], b3[TILE_BYTES];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
   const int tiles_m = (p.M + BM - 1) / BM;
@@ -281,11 +318,8 @@ __global__ void __launch_bounds__(NT) gemm_kernel(GemmParams p) {
   const int tm = first_m + (pid % group) % gm;
   const int tn = (pid % group) / gm;
   const int m0 = tm * BM, n0 = tn * BN;
-
   const int wm = wave >> 2, wn = wave & 3;
-  constexpr int PW = PAIR / 32;
-  const int c0 = (wn / PW) * (2 * PAIR) + (wn % PW) * 32;
-  const int c1 = c0 + PAIR;
+  const int ncol[2] = {lo_col<PAIR>(wn), lo_col<PAIR>(wn) + PAIR};
 
   f32x16 acc[4][2];
 #pragma unroll
@@ -293,54 +327,82 @@ __global__ void __launch_bounds__(NT) gemm_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
-  const bool loads_a = tid < 256;
-  const int ltid = tid & 255;
-  const int nk = (p.K + BK - 1) / BK;
-  u32x4 stage[8];
+  uint32_t ra = 0, rb = 0;
+  if constexpr (LA == Layout::KC) ra = kc_row(p.A, m0, tm, wave, lane);
+  if constexpr (LB == Layout::KC) rb = kc_row(p.B, n0, tn, wave, lane);
 
-  auto gload = [&](int kt) {
-    if (loads_a) load_block<LA>(p.A, m0, tm, kt * BK, p.K, ltid, stage);
-    else load_block<LB>(p.B, n0, tn, kt * BK, p.K, ltid, stage);
+  auto issue = [&](int k0, uint8_t* la, uint8_t* lb) {
+    if constexpr (LA == Layout::KC) copy_kc(la, p.A, ra, k0, p.K, wave, lane);
+    else copy_mn(la, p.A, m0, k0, p.K, wave, lane);
+    if constexpr (LB == Layout::KC) copy_kc(lb, p.B, rb, k0, p.K, wave, lane);
+    else copy_mn(lb, p.B, n0, k0, p.K, wave, lane);
   };
-  auto lstore = [&](int buf) {
-    uint8_t* base = smem + buf * 2 * TILE_BYTES;
-    if (loads_a) store_block<LA>(base, ltid, stage);
-    else store_block<LB>(base + TILE_BYTES, ltid, stage);
-  };
-
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    const uint8_t* sa = smem + buf * 2 * TILE_BYTES;
-    const uint8_t* sb = sa + TILE_BYTES;
+  auto compute = [&](int k0, const uint8_t* la, const uint8_t* lb) {
+    const bool tail = k0 + BK > p.K;     // uniform: only the last step of a ragged K
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      const int ch = kk * 2 + (lane >> 5);
       bf16x8 af[4], bf[2];
 #pragma unroll
-      for (int ms = 0; ms < 4; ++ms)
-        af[ms] = *reinterpret_cast<const bf16x8*>(sa + lds_off(wm * 128 + ms * 32 + (lane & 31), ch));
-      bf[0] = *reinterpret_cast<const bf16x8*>(sb + lds_off(c0 + (lane & 31), ch));
-      bf[1] = *reinterpret_cast<const bf16x8*>(sb + lds_off(c1 + (lane & 31), ch));
+      for (int ms = 0; ms < 4; ++ms) af[ms] = frag<LA>(la, wm * 128 + ms * 32, kk, lane);
+#pragma unroll
+      for (int ns = 0; ns < 2; ++ns) bf[ns] = frag<LB>(lb, ncol[ns], kk, lane);
+      if (tail) {
+        const bool z = k0 + 16 * kk + 8 * (lane >> 5) >= p.K;
+#pragma unroll
+        for (int ms = 0; ms < 4; ++ms) af[ms] = z ? bf16x8{} : af[ms];
+#pragma unroll
+        for (int ns = 0; ns < 2; ++ns) bf[ns] = z ? bf16x8{} : bf[ns];
+      }
 #pragma unroll
       for (int ms = 0; ms < 4; ++ms)
 #pragma unroll
         for (int ns = 0; ns < 2; ++ns)
           acc[ms][ns] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ms], bf[ns], acc[ms][ns], 0, 0, 0);
     }
-    if (kt + 1 < nk) lstore(buf ^ 1);
-    __syncthreads();
-  }
+  };
 
-  // Epilogue: stage each wave's 128x64 block (two 64-row halves) as fp32 in
-  // LDS, then hand out 8-column vectors.  MFMA 32x32 output layout: register i
-  // of lane l is row 8*(i/4) + 4*(l/32) + i%4, column l%32.
-  float* st = reinterpret_cast<float*>(smem) + wave * STAGE_WAVE;
+  // Step kt reads stage kt % 4.  On entry to a step, the copies of the next two
+  // steps may still be in flight (4 wave instructions each): wait until only
+  // those remain, then a barrier makes every wave's copy of this step visible
+  // and frees the stage of step kt - 1 for the copy of step kt + 3.
+  const int nk = (p.K + BK - 1) / BK;
+  auto step = [&](int kt, const uint8_t* la, const uint8_t* lb, uint8_t* na, uint8_t* nb) {
+    const int after = nk - 1 - kt;
+    if (after >= 2) wait_vm<8>();
+    else if (after == 1) wait_vm<4>();
+    else wait_vm<0>();
+    __syncthreads();
+    if (kt + 3 < nk) issue((kt + 3) * BK, na, nb);
+    compute(kt * BK, la, lb);
+    __builtin_amdgcn_sched_barrier(0);   // keep the steps apart (register pressure)
+  };
+  issue(0, a0, b0);
+  if (nk > 1) issue(BK, a1, b1);
+  if (nk > 2) issue(2 * BK, a2, b2);
+  // Whole groups of 4 steps without early exits (an exit between the unrolled
+  // steps makes the register allocator spill), then the remaining 0-3 steps.
+  int kt = 0;
+  for (; kt + 4 <= nk; kt += 4) {
+    step(kt, a0, b0, a3, b3);
+    step(kt + 1, a1, b1, a0, b0);
+    step(kt + 2, a2, b2, a1, b1);
+    step(kt + 3, a3, b3, a2, b2);
+  }
+  const int rest = nk - kt;
+  if (rest > 0) step(kt, a0, b0, a3, b3);
+  if (rest > 1) step(kt + 1, a1, b1, a0, b0);
+  if (rest > 2) step(kt + 2, a2, b2, a1, b1);
+  __syncthreads();   // every wave is done reading the stages before they become staging space
+
+  // Epilogue: two passes of 64 rows; wave w stages its 64 x 64 fp32 block in
+  // LDS buffer w (column halves swapped on rows with bit 2 set, so the two
+  // half-waves write different banks).  Accumulator register i of a lane: row
+  // 8(i/4) + 4(lane/32) + i%4, column lane%32 of its 32x32 tile.
+  uint8_t* mine = wave == 0 ? a0 : wave == 1 ? b0 : wave == 2 ? a1 : wave == 3 ? b1
+                : wave == 4 ? a2 : wave == 5 ? b2 : wave == 6 ? a3 : b3;
+  float* st = reinterpret_cast<float*>(mine);
 #pragma unroll
-  for (int ph = 0; ph < 2; ++ph) {
+  for (int pass = 0; pass < 2; ++pass) {
 #pragma unroll
     for (int mm = 0; mm < 2; ++mm)
 #pragma unroll
@@ -348,38 +410,33 @@ __global__ void __launch_bounds__(NT) gemm_kernel(GemmParams p) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int r = mm * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-          st[r * STAGE_LD + ns * 32 + (lane & 31)] = acc[2 * ph + mm][ns][i];
+          const int cc = (ns * 32 + (lane & 31)) ^ (((r >> 2) & 1) << 4);
+          st[r * 64 + cc] = acc[2 * pass + mm][ns][i];
         }
-    __syncthreads();
-#pragma unroll
-    for (int pass = 0; pass < 4; ++pass) {
-      const int rr = pass * 16 + (lane >> 2);
-      const int cc = (lane & 3) * 8;
-      float lo[8], hi[8];
-      const float* srow = st + rr * STAGE_LD + cc;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        lo[j] = srow[j];
-        hi[j] = srow[32 + j];
-      }
-      const int64_t m = static_cast<int64_t>(m0) + wm * 128 + ph * 64 + rr;
-      epilogue<PAIR>(p, m, tn, c0 + cc, lo, hi);
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+#pragma unroll 1
+    for (int it = 0; it < 4; ++it) {
+      const int idx = it * 64 + lane;
+      const int rr = idx >> 2, c8 = (idx & 3) * 8;   // staged row, 8-column vector of the low block
+      const int flip = ((rr >> 2) & 1) << 4;
+      const float4* lo4 = reinterpret_cast<const float4*>(st + rr * 64 + (c8 ^ flip));
+      const float4* hi4 = reinterpret_cast<const float4*>(st + rr * 64 + ((32 + c8) ^ flip));
+      const float4 l0 = lo4[0], l1 = lo4[1], h0 = hi4[0], h1 = hi4[1];
+      float lo[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
+      float hi[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+      const int64_t m = static_cast<int64_t>(m0) + wm * 128 + pass * 64 + rr;
+      epilogue<KIND, PAIR>(p, m, tn, ncol[0] + c8, lo, hi);
     }
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0xc07f);
   }
   (void)n0;
 }
 
-template <Layout LA, Layout LB>
-hipError_t launch(const GemmParams& p, int pair, hipStream_t stream) {
+template <Layout LA, Layout LB, EpiKind KIND, int PAIR>
+hipError_t launch(const GemmParams& p, hipStream_t stream) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = p.B.split_rows ? (p.B.split_rows + 127) / 128 : (p.N + BN - 1) / BN;
-  const dim3 grid(tiles_m * tiles_n), block(NT);
-  switch (pair) {
-    case 32: hipLaunchKernelGGL((gemm_kernel<LA, LB, 32>), grid, block, 0, stream, p); break;
-    case 64: hipLaunchKernelGGL((gemm_kernel<LA, LB, 64>), grid, block, 0, stream, p); break;
-    default: hipLaunchKernelGGL((gemm_kernel<LA, LB, 128>), grid, block, 0, stream, p); break;
-  }
+  hipLaunchKernelGGL((gemm_kernel<LA, LB, KIND, PAIR>), dim3(tiles_m * tiles_n), dim3(NT), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -387,12 +444,23 @@ hipError_t launch(const GemmParams& p, int pair, hipStream_t stream) {
 
 hipError_t gemm(const GemmParams& p, Layout la, Layout lb, hipStream_t stream) {
   if (p.M <= 0 || p.N <= 0 || p.K <= 0) return hipSuccess;
-  int pair = 128;
-  if (p.epi.kind == EpiKind::QkvRope) pair = p.epi.d_h / 2;
-  if (la == Layout::KC && lb == Layout::KC) return launch<Layout::KC, Layout::KC>(p, pair, stream);
-  if (la == Layout::KC && lb == Layout::MN) return launch<Layout::KC, Layout::MN>(p, pair, stream);
-  if (la == Layout::MN && lb == Layout::MN) return launch<Layout::MN, Layout::MN>(p, pair, stream);
-  return launch<Layout::MN, Layout::KC>(p, pair, stream);
+  using L = Layout;
+  using E = EpiKind;
+  const E k = p.epi.kind;
+  if (la == L::KC && lb == L::KC) {
+    if (k == E::QkvRope && p.epi.d_h == 128) return launch<L::KC, L::KC, E::QkvRope, 64>(p, stream);
+    if (k == E::QkvRope && p.epi.d_h == 64) return launch<L::KC, L::KC, E::QkvRope, 32>(p, stream);
+    if (k == E::ResidualSP) return launch<L::KC, L::KC, E::ResidualSP, 128>(p, stream);
+    if (k == E::SwiGLUFwd) return launch<L::KC, L::KC, E::SwiGLUFwd, 128>(p, stream);
+    if (k == E::StoreBF16) return launch<L::KC, L::KC, E::StoreBF16, 128>(p, stream);
+  } else if (la == L::KC && lb == L::MN) {
+    if (k == E::SwiGLUBwd) return launch<L::KC, L::MN, E::SwiGLUBwd, 128>(p, stream);
+    if (k == E::ResidualSP) return launch<L::KC, L::MN, E::ResidualSP, 128>(p, stream);
+    if (k == E::StoreBF16) return launch<L::KC, L::MN, E::StoreBF16, 128>(p, stream);
+  } else if (la == L::MN && lb == L::MN) {
+    if (k == E::AccF32) return launch<L::MN, L::MN, E::AccF32, 128>(p, stream);
+  }
+  return hipErrorInvalidValue;     // a layout / epilogue pairing the layer never uses
 }
 
 }  // namespace l4d

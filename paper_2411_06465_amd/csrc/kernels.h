@@ -23,14 +23,21 @@ struct RowSrc {
   __host__ __device__ static RowSrc plain(const void* p, int64_t ld) {
     return RowSrc{static_cast<const uint16_t*>(p), nullptr, ld, 1, 1, 0, 1};
   }
+  // Row m as (index into own) or (index into peer) | 0x80000000; 32-bit arithmetic
+  // (row counts are validated below 2^30 on the host).
+  __device__ inline uint32_t row_index(int64_t m64) const {
+    const int32_t m = static_cast<int32_t>(m64);
+    if (t == 1) return static_cast<uint32_t>(m);
+    const int32_t bi = m / s_c;
+    const int32_t i = m - bi * s_c;
+    const int32_t lo = r * s_sp;
+    if (i >= lo && i < lo + s_sp) return static_cast<uint32_t>(bi * s_sp + (i - lo));
+    const int32_t pi = i < lo ? i : i - s_sp;
+    return static_cast<uint32_t>(bi * (t - 1) * s_sp + pi) | 0x80000000u;
+  }
   __device__ inline const uint16_t* row(int64_t m) const {
-    if (t == 1) return own + m * ld;
-    int64_t bi = m / s_c;
-    int32_t i = static_cast<int32_t>(m - bi * s_c);
-    int32_t lo = r * s_sp;
-    if (i >= lo && i < lo + s_sp) return own + (bi * s_sp + (i - lo)) * ld;
-    int32_t pi = i < lo ? i : i - s_sp;
-    return peer + (bi * static_cast<int64_t>(t - 1) * s_sp + pi) * ld;
+    const uint32_t o = row_index(m);
+    return ((o & 0x80000000u) ? peer : own) + static_cast<int64_t>(o & 0x7fffffffu) * ld;
   }
 };
 
@@ -162,7 +169,8 @@ struct AttnParams {
 // Number of query-head slices the dK/dV pass uses for this shape (1 = none).
 int attn_bwd_splits(const AttnParams& p);
 hipError_t attn_fwd(const AttnParams& p, hipStream_t stream);
-hipError_t attn_bwd(const AttnParams& p, hipStream_t stream);
+// part 0: delta = rowsum(dO * O); 1: dK, dV (+ slice reduction); 2: dQ.
+hipError_t attn_bwd(const AttnParams& p, int part, hipStream_t stream);
 
 // ---------------------------------------------------------------- cross-entropy
 
