@@ -24,6 +24,8 @@
 // n + PAIR land in the same lane and register: a RoPE pair (i, i + d_h/2) or a
 // gate/up pair of the fused FFN weight.  The epilogue stages 64 rows at a time
 // through LDS and hands 8-column vectors to the fused operation.
+#include <stdlib.h>
+
 #include "kernels.h"
 
 namespace l4d {
@@ -38,7 +40,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #define GPTR(p) ((const __attribute__((address_space(1))) void*)(p))
 #define LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
-constexpr int BM = 256, BN = 256, BK = 32, NT = 512;
+constexpr int BM = 256, BN = 256, BK = 32;
 constexpr int TILE_BYTES = 256 * BK * 2;     // 16 KB per operand per stage
 constexpr int GROUP_M = 8;
 
@@ -73,45 +75,60 @@ __device__ __forceinline__ int kc_off(int row, int chunk) {
 __device__ __forceinline__ int mn_swz(int row) { return (row & 3) << 1; }
 __device__ __forceinline__ int mn_off(int row, int chunk) { return row * 512 + ((chunk ^ mn_swz(row)) << 4); }
 
-// Each wave copies LDS KB number kb = wave and wave + 8 of both operand tiles.
-// KC: KB kb holds sub-block kb/8, rows 32*(kb%8) + lane/2 -- the same tile row
-// for both of a lane's copies, fixed over K.  Its source row is kept as a
-// 32-bit element offset, bit 31 selecting the peer base of a
-// sequence-parallel gather.
-__device__ __forceinline__ uint32_t kc_row(const Operand& op, int x0, int tile_idx, int wave, int lane) {
-  const int xr = 32 * wave + (lane >> 1);
-  int64_t gx;
-  if (op.split_rows) {
-    int i = tile_idx * 128 + (xr & 127);
-    if (i >= op.split_rows) i = op.split_rows - 1;
-    gx = (xr >= 128 ? op.split_off : 0) + i;
-  } else {
-    gx = x0 + xr;
-    if (gx >= op.rows) gx = op.rows - 1;
+// Each stage holds 16 KB per operand; wave w copies LDS KB numbers
+// kb = w + WAVES * q.  KC: KB kb holds sub-block kb/8 and tile rows
+// 32 * (kb % 8) + lane/2, so a lane's source rows are fixed over K; they are
+// kept as 32-bit element offsets, bit 31 selecting the peer base of a
+// sequence-parallel gather.  MN: KB kb holds k-rows 2 kb + lane/32.
+template <int WAVES>
+struct KcRows {
+  uint32_t off[8 / WAVES];   // one per distinct row block kb % 8 of this wave
+};
+
+template <int WAVES>
+__device__ __forceinline__ KcRows<WAVES> kc_rows(const Operand& op, int x0, int tile_idx, int wave, int lane) {
+  KcRows<WAVES> r;
+#pragma unroll
+  for (int j = 0; j < 8 / WAVES; ++j) {
+    const int xr = 32 * (wave + WAVES * j) + (lane >> 1);
+    int64_t gx;
+    if (op.split_rows) {
+      int i = tile_idx * 128 + (xr & 127);
+      if (i >= op.split_rows) i = op.split_rows - 1;
+      gx = (xr >= 128 ? op.split_off : 0) + i;
+    } else {
+      gx = x0 + xr;
+      if (gx >= op.rows) gx = op.rows - 1;
+    }
+    r.off[j] = op.src.row_index(gx);
   }
-  return op.src.row_index(gx);
+  return r;
 }
 
-__device__ __forceinline__ void copy_kc(uint8_t* lds, const Operand& op, uint32_t row_off, int k0, int K, int wave,
-                                        int lane) {
-  const int row = 32 * wave + (lane >> 1);
-  const uint16_t* base = ((row_off & 0x80000000u) ? op.src.peer : op.src.own) +
-                         static_cast<int64_t>(row_off & 0x7fffffffu) * op.src.ld;
+template <int WAVES>
+__device__ __forceinline__ void copy_kc(uint8_t* lds, const Operand& op, const KcRows<WAVES>& rows, int k0, int K,
+                                        int wave, int lane) {
 #pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
+  for (int q = 0; q < 16 / WAVES; ++q) {
+    const int kb = wave + WAVES * q;
+    const int kk = kb >> 3;
+    const int row = 32 * (kb & 7) + (lane >> 1);
+    const uint32_t o = rows.off[q % (8 / WAVES)];
+    const uint16_t* base = ((o & 0x80000000u) ? op.src.peer : op.src.own) +
+                           static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld;
     const int hh = (lane & 1) ^ ((row >> 2) & 1);
     int k = k0 + kk * 16 + hh * 8;
     if (k >= K) k = K - 8;            // those fragments are zeroed before use
-    __builtin_amdgcn_global_load_lds(GPTR(base + k), LPTR(lds + (wave + 8 * kk) * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(GPTR(base + k), LPTR(lds + kb * 1024), 16, 0, 0);
   }
 }
 
-// MN: KB kb holds k-rows 2 kb + lane/32.
+template <int WAVES>
 __device__ __forceinline__ void copy_mn(uint8_t* lds, const Operand& op, int x0, int k0, int K, int wave,
                                         int lane) {
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int kb = wave + 8 * q;
+  for (int q = 0; q < 16 / WAVES; ++q) {
+    const int kb = wave + WAVES * q;
     const int kr = 2 * kb + (lane >> 5);
     const int lc = (lane & 31) ^ mn_swz(kr);
     int k = k0 + kr;
@@ -287,24 +304,45 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn,
   }
 }
 
-// Tile column of a wave's low 32-column block (wn = 0..3); its partner is PAIR further.
-template <int PAIR>
-__device__ __forceinline__ int lo_col(int wn) {
-  constexpr int PW = PAIR / 32;
-  return (wn / PW) * (2 * PAIR) + (wn % PW) * 32;
+// Tile column of a wave's low 32-column block j; its partner is PAIR further.
+// 8 waves: wn = 0..3, one low block each; 4 waves: wn = 0..1, two each.
+template <int WAVES, int PAIR>
+__device__ __forceinline__ int lo_col(int wn, int j) {
+  if constexpr (WAVES == 8) {
+    constexpr int PW = PAIR / 32;
+    return (wn / PW) * (2 * PAIR) + (wn % PW) * 32;
+  } else {
+    if constexpr (PAIR == 32) return wn * 128 + j * 64;
+    else if constexpr (PAIR == 64) return wn * 128 + j * 32;
+    else return wn * 64 + j * 32;
+  }
 }
 
 // -------------------------------------------------------------- the kernel
+
+// Workgroup barrier between pipeline steps.  __syncthreads() would also fence
+// global memory, i.e. wait for every copy still in flight -- including the
+// stages being prefetched; each wave has already waited for its own copies of
+// the step that is about to be read, so only the LDS reads of the previous
+// step (lgkmcnt) must drain before the barrier.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 template <int N>
 __device__ __forceinline__ void wait_vm() {
   if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-  else asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
 }
 
-template <Layout LA, Layout LB, EpiKind KIND, int PAIR>
-__global__ void __launch_bounds__(NT, 1) gemm_kernel(GemmParams p) {  // 8 waves: 2 per SIMD
+template <Layout LA, Layout LB, EpiKind KIND, int PAIR, int WAVES>
+__global__ void __launch_bounds__(WAVES * 64, 1) gemm_kernel(GemmParams p) {
+  constexpr int NS = WAVES == 8 ? 2 : 4;     // 32-column blocks per wave (half of them low)
+  constexpr int PER = 16 / WAVES;           // copies per operand per stage per wave
   __shared__ __attribute__((aligned(16))) uint8_t a0[TILE_BYTES], b0[TILE_BYTES], a1[TILE_BYTES], b1[TILE_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t a2[TILE_BYTES], b2[TILE_BYTES], a3[TILE_BYTES], b3[TILE_BYTES];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -318,63 +356,68 @@ __global__ void __launch_bounds__(NT, 1) gemm_kernel(GemmParams p) {  // 8 waves
   const int tm = first_m + (pid % group) % gm;
   const int tn = (pid % group) / gm;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int wm = wave >> 2, wn = wave & 3;
-  const int ncol[2] = {lo_col<PAIR>(wn), lo_col<PAIR>(wn) + PAIR};
+  const int wm = WAVES == 8 ? (wave >> 2) : (wave >> 1);
+  const int wn = WAVES == 8 ? (wave & 3) : (wave & 1);
+  int ncol[NS];
+#pragma unroll
+  for (int j = 0; j < NS / 2; ++j) {
+    ncol[j] = lo_col<WAVES, PAIR>(wn, j);
+    ncol[j + NS / 2] = ncol[j] + PAIR;
+  }
 
-  f32x16 acc[4][2];
+  f32x16 acc[4][NS];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
 
-  uint32_t ra = 0, rb = 0;
-  if constexpr (LA == Layout::KC) ra = kc_row(p.A, m0, tm, wave, lane);
-  if constexpr (LB == Layout::KC) rb = kc_row(p.B, n0, tn, wave, lane);
+  KcRows<WAVES> ra{}, rb{};
+  if constexpr (LA == Layout::KC) ra = kc_rows<WAVES>(p.A, m0, tm, wave, lane);
+  if constexpr (LB == Layout::KC) rb = kc_rows<WAVES>(p.B, n0, tn, wave, lane);
 
   auto issue = [&](int k0, uint8_t* la, uint8_t* lb) {
-    if constexpr (LA == Layout::KC) copy_kc(la, p.A, ra, k0, p.K, wave, lane);
-    else copy_mn(la, p.A, m0, k0, p.K, wave, lane);
-    if constexpr (LB == Layout::KC) copy_kc(lb, p.B, rb, k0, p.K, wave, lane);
-    else copy_mn(lb, p.B, n0, k0, p.K, wave, lane);
+    if constexpr (LA == Layout::KC) copy_kc<WAVES>(la, p.A, ra, k0, p.K, wave, lane);
+    else copy_mn<WAVES>(la, p.A, m0, k0, p.K, wave, lane);
+    if constexpr (LB == Layout::KC) copy_kc<WAVES>(lb, p.B, rb, k0, p.K, wave, lane);
+    else copy_mn<WAVES>(lb, p.B, n0, k0, p.K, wave, lane);
   };
   auto compute = [&](int k0, const uint8_t* la, const uint8_t* lb) {
     const bool tail = k0 + BK > p.K;     // uniform: only the last step of a ragged K
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 af[4], bf[2];
+      bf16x8 af[4], bf[NS];
 #pragma unroll
       for (int ms = 0; ms < 4; ++ms) af[ms] = frag<LA>(la, wm * 128 + ms * 32, kk, lane);
 #pragma unroll
-      for (int ns = 0; ns < 2; ++ns) bf[ns] = frag<LB>(lb, ncol[ns], kk, lane);
+      for (int ns = 0; ns < NS; ++ns) bf[ns] = frag<LB>(lb, ncol[ns], kk, lane);
       if (tail) {
         const bool z = k0 + 16 * kk + 8 * (lane >> 5) >= p.K;
 #pragma unroll
         for (int ms = 0; ms < 4; ++ms) af[ms] = z ? bf16x8{} : af[ms];
 #pragma unroll
-        for (int ns = 0; ns < 2; ++ns) bf[ns] = z ? bf16x8{} : bf[ns];
+        for (int ns = 0; ns < NS; ++ns) bf[ns] = z ? bf16x8{} : bf[ns];
       }
 #pragma unroll
       for (int ms = 0; ms < 4; ++ms)
 #pragma unroll
-        for (int ns = 0; ns < 2; ++ns)
+        for (int ns = 0; ns < NS; ++ns)
           acc[ms][ns] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ms], bf[ns], acc[ms][ns], 0, 0, 0);
     }
   };
 
-  // Step kt reads stage kt % 4.  On entry to a step, the copies of the next two
-  // steps may still be in flight (4 wave instructions each): wait until only
-  // those remain, then a barrier makes every wave's copy of this step visible
-  // and frees the stage of step kt - 1 for the copy of step kt + 3.
+  // Step kt reads stage kt % 4.  On entry to a step the copies of the next two
+  // steps may still be in flight (2 * PER instructions per operand each):
+  // wait until only those remain, then a barrier makes every wave's copy of
+  // this step visible and frees the stage of step kt - 1 for step kt + 3.
   const int nk = (p.K + BK - 1) / BK;
   auto step = [&](int kt, const uint8_t* la, const uint8_t* lb, uint8_t* na, uint8_t* nb) {
     const int after = nk - 1 - kt;
-    if (after >= 2) wait_vm<8>();
-    else if (after == 1) wait_vm<4>();
+    if (after >= 2) wait_vm<4 * PER>();
+    else if (after == 1) wait_vm<2 * PER>();
     else wait_vm<0>();
-    __syncthreads();
+    stage_barrier();
     if (kt + 3 < nk) issue((kt + 3) * BK, na, nb);
     compute(kt * BK, la, lb);
-    __builtin_amdgcn_sched_barrier(0);   // keep the steps apart (register pressure)
   };
   issue(0, a0, b0);
   if (nk > 1) issue(BK, a1, b1);
@@ -394,49 +437,65 @@ __global__ void __launch_bounds__(NT, 1) gemm_kernel(GemmParams p) {  // 8 waves
   if (rest > 2) step(kt + 2, a2, b2, a1, b1);
   __syncthreads();   // every wave is done reading the stages before they become staging space
 
-  // Epilogue: two passes of 64 rows; wave w stages its 64 x 64 fp32 block in
-  // LDS buffer w (column halves swapped on rows with bit 2 set, so the two
-  // half-waves write different banks).  Accumulator register i of a lane: row
-  // 8(i/4) + 4(lane/32) + i%4, column lane%32 of its 32x32 tile.
-  uint8_t* mine = wave == 0 ? a0 : wave == 1 ? b0 : wave == 2 ? a1 : wave == 3 ? b1
-                : wave == 4 ? a2 : wave == 5 ? b2 : wave == 6 ? a3 : b3;
+  // Epilogue: each wave stages R rows x (NS*32) columns of fp32 at a time in
+  // its own 16 KB of LDS (column halves swapped on rows with bit 2 set, so the
+  // two half-waves write different banks) and hands out 8-column vectors of
+  // its low blocks with their PAIR partners.  Accumulator register i of a
+  // lane: row 8(i/4) + 4(lane/32) + i%4, column lane%32 of its 32x32 tile.
+  constexpr int C = NS * 32, R = 4096 / C, PASSES = 128 / R, MS_PER = R / 32;
+  const int sb = WAVES == 8 ? wave : 2 * wave;    // this wave's 16 KB staging buffer
+  uint8_t* mine = sb == 0 ? a0 : sb == 1 ? b0 : sb == 2 ? a1 : sb == 3 ? b1 : sb == 4 ? a2 : sb == 5 ? b2
+                : sb == 6 ? a3 : b3;
   float* st = reinterpret_cast<float*>(mine);
 #pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
+  for (int pass = 0; pass < PASSES; ++pass) {
 #pragma unroll
-    for (int mm = 0; mm < 2; ++mm)
+    for (int mm = 0; mm < MS_PER; ++mm)
 #pragma unroll
-      for (int ns = 0; ns < 2; ++ns)
+      for (int ns = 0; ns < NS; ++ns)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int r = mm * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
           const int cc = (ns * 32 + (lane & 31)) ^ (((r >> 2) & 1) << 4);
-          st[r * 64 + cc] = acc[2 * pass + mm][ns][i];
+          st[r * C + cc] = acc[pass * MS_PER + mm][ns][i];
         }
     __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+    constexpr int VEC = R * (NS / 2) * 4;  // 8-column vectors of the low blocks per pass
 #pragma unroll 1
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < VEC / 64; ++it) {
       const int idx = it * 64 + lane;
-      const int rr = idx >> 2, c8 = (idx & 3) * 8;   // staged row, 8-column vector of the low block
+      const int rr = idx / ((NS / 2) * 4), v = idx % ((NS / 2) * 4);
+      const int j = v >> 2, c8 = (v & 3) * 8;
       const int flip = ((rr >> 2) & 1) << 4;
-      const float4* lo4 = reinterpret_cast<const float4*>(st + rr * 64 + (c8 ^ flip));
-      const float4* hi4 = reinterpret_cast<const float4*>(st + rr * 64 + ((32 + c8) ^ flip));
+      const float4* lo4 = reinterpret_cast<const float4*>(st + rr * C + ((j * 32 + c8) ^ flip));
+      const float4* hi4 = reinterpret_cast<const float4*>(st + rr * C + (((j + NS / 2) * 32 + c8) ^ flip));
       const float4 l0 = lo4[0], l1 = lo4[1], h0 = hi4[0], h1 = hi4[1];
       float lo[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
       float hi[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
-      const int64_t m = static_cast<int64_t>(m0) + wm * 128 + pass * 64 + rr;
-      epilogue<KIND, PAIR>(p, m, tn, ncol[0] + c8, lo, hi);
+      const int64_t m = static_cast<int64_t>(m0) + wm * 128 + pass * R + rr;
+      epilogue<KIND, PAIR>(p, m, tn, ncol[j] + c8, lo, hi);
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);
   }
   (void)n0;
 }
 
+int gemm_waves() {
+  static int w = [] {
+    const char* e = getenv("L4D_GEMM_WAVES");
+    return (e && atoi(e) == 4) ? 4 : 8;
+  }();
+  return w;
+}
+
 template <Layout LA, Layout LB, EpiKind KIND, int PAIR>
 hipError_t launch(const GemmParams& p, hipStream_t stream) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = p.B.split_rows ? (p.B.split_rows + 127) / 128 : (p.N + BN - 1) / BN;
-  hipLaunchKernelGGL((gemm_kernel<LA, LB, KIND, PAIR>), dim3(tiles_m * tiles_n), dim3(NT), 0, stream, p);
+  if (gemm_waves() == 4)
+    hipLaunchKernelGGL((gemm_kernel<LA, LB, KIND, PAIR, 4>), dim3(tiles_m * tiles_n), dim3(256), 0, stream, p);
+  else
+    hipLaunchKernelGGL((gemm_kernel<LA, LB, KIND, PAIR, 8>), dim3(tiles_m * tiles_n), dim3(512), 0, stream, p);
   return hipGetLastError();
 }
 
