@@ -1,29 +1,36 @@
 // bf16 GEMM on the gfx950 matrix cores: C[m][n] = sum_k A(m,k) B(n,k), fp32
 // accumulation, with the layer's fused epilogues.
 //
-// Tiling: a 512-thread workgroup (8 waves, two per SIMD) owns a 256x256 tile
-// of C; each wave accumulates a 128x64 block as 4 x 2 tiles of
-// v_mfma_f32_32x32x16_bf16 (128 accumulator registers).  K advances in steps
-// of 32 through a 4-stage pipeline: operand tiles are copied global -> LDS by
-// global_load_lds_dwordx4 (one contiguous KB per wave instruction, no staging
-// registers) three steps ahead of their use.  Every stage buffer is its own
-// LDS object so the compiler knows a read of one stage cannot depend on the
-// copies still landing in the others.
+// A workgroup owns a 256x256 tile of C; each wave accumulates a 128 x (NS*32)
+// block as tiles of v_mfma_f32_32x32x16_bf16.  Operand tiles move global ->
+// LDS by global_load_lds_dwordx4 (direct-to-LDS DMA, one contiguous KB per
+// wave instruction, no staging registers).  Every stage buffer is its own LDS
+// object, so the compiler knows a read of one stage cannot depend on the
+// copies still landing in the others.  Two kernels:
+//
+//  * gemm_bk64 (K a multiple of 128): two stages of 64 k.  A K-contiguous copy
+//    moves 8 whole 128-byte rows per instruction (one cache line each); the
+//    fragments of the next 16-k sub-step are read from LDS under the MFMAs of
+//    the current one, and the barrier that publishes stage kt+1 sits before
+//    the last sub-step of stage kt, right after which the freed buffers take
+//    stage kt+2.  8 waves (two per SIMD, 128x64 each) or 4 (128x128 each).
+//  * gemm_bk32 (any K that is a multiple of 8): 8 waves, four stages of 32 k,
+//    16 rows x 64 bytes per copy instruction, the stage past K zeroed in
+//    registers.
 //
 // Operand layouts: "KC" (reduction index contiguous: activations in the
-// forward, the output gradient in dX) is stored as two 16-k sub-blocks of
-// 256 rows x 32 bytes, the two halves of a row swapped on rows with bit 2
-// set: the 8 rows one fragment read touches fall in 8 different bank groups
-// and every fragment address is a per-lane base plus an immediate.  "MN"
-// (reduction index strided: the weight in dX, both operands of dW) is stored
-// as 32 k-rows x 256 columns with the 16-byte chunks XOR-swizzled by row, and
-// read with two ds_read_b64_tr_b16 that hand each lane 4 consecutive k of one
-// column -- the transpose happens in the LDS read, not in registers.
+// forward, the output gradient in dX) is stored row by row, the 16-byte chunks
+// of a row permuted by an XOR with low row bits so that the 8 rows an 8-lane
+// group of a fragment read touches cover all 32 banks.  "MN" (reduction
+// index strided: the weight in dX, both operands of dW) is stored as k-rows
+// of 256 columns with the 16-byte chunks XOR-swizzled by row, and read with
+// two ds_read_b64_tr_b16 that hand each lane 4 consecutive k of one column --
+// the transpose happens in the LDS read, not in registers.
 //
-// A wave's two 32-column blocks sit PAIR columns apart, so the columns n and
-// n + PAIR land in the same lane and register: a RoPE pair (i, i + d_h/2) or a
-// gate/up pair of the fused FFN weight.  The epilogue stages 64 rows at a time
-// through LDS and hands 8-column vectors to the fused operation.
+// A wave's 32-column blocks come in pairs PAIR columns apart, so the columns
+// n and n + PAIR land in the same lane and register: a RoPE pair (i, i + d_h/2)
+// or a gate/up pair of the fused FFN weight.  The epilogue stages rows through
+// LDS and hands 8-column vectors to the fused operation.
 #include <stdlib.h>
 
 #include "kernels.h"
@@ -67,30 +74,33 @@ __device__ __forceinline__ int xcd_remap(int bid, int nwg) {
 }
 
 // ------------------------------------------------------------------ LDS layouts
-// KC tile: 16-byte chunk c (0..3) of row r (0..255) in sub-block c/2.
-__device__ __forceinline__ int kc_off(int row, int chunk) {
-  return (chunk >> 1) * 8192 + row * 32 + (((chunk & 1) ^ ((row >> 2) & 1)) << 4);
-}
+// KC tile: row r (0..255) holds its 32 k (64 bytes) at r*64, the four 16-byte
+// chunks permuted by c ^ ((r >> 1) & 3): the 8 rows one 8-lane group of a
+// fragment read touches then cover all 32 banks once.
+__device__ __forceinline__ int kc_off(int row, int chunk) { return row * 64 + ((chunk ^ ((row >> 1) & 3)) << 4); }
 // MN tile: k-row r (0..31), 16-byte chunk c (0..31) of its 256 columns.
 __device__ __forceinline__ int mn_swz(int row) { return (row & 3) << 1; }
 __device__ __forceinline__ int mn_off(int row, int chunk) { return row * 512 + ((chunk ^ mn_swz(row)) << 4); }
 
 // Each stage holds 16 KB per operand; wave w copies LDS KB numbers
-// kb = w + WAVES * q.  KC: KB kb holds sub-block kb/8 and tile rows
-// 32 * (kb % 8) + lane/2, so a lane's source rows are fixed over K; they are
-// kept as 32-bit element offsets, bit 31 selecting the peer base of a
-// sequence-parallel gather.  MN: KB kb holds k-rows 2 kb + lane/32.
+// kb = w + WAVES * q.  KC: KB kb holds tile rows 16 kb + lane/4, 64 contiguous
+// bytes of each row per instruction (4 lanes), lane l fetching the chunk
+// that belongs at its LDS slot l % 4: chunk (l & 3) ^ ((l >> 3) & 3), the
+// same for every q.  A lane's source rows are fixed over K and kept as
+// pointers.  MN: KB kb holds k-rows 2 kb + lane/32.
 template <int WAVES>
 struct KcRows {
-  uint32_t off[8 / WAVES];   // one per distinct row block kb % 8 of this wave
+  const uint16_t* row[16 / WAVES];   // source row of copy q (chunk not included)
+  int c8;                            // element offset of the lane's chunk
 };
 
 template <int WAVES>
 __device__ __forceinline__ KcRows<WAVES> kc_rows(const Operand& op, int x0, int tile_idx, int wave, int lane) {
   KcRows<WAVES> r;
+  r.c8 = 8 * ((lane & 3) ^ ((lane >> 3) & 3));
 #pragma unroll
-  for (int j = 0; j < 8 / WAVES; ++j) {
-    const int xr = 32 * (wave + WAVES * j) + (lane >> 1);
+  for (int q = 0; q < 16 / WAVES; ++q) {
+    const int xr = 16 * (wave + WAVES * q) + (lane >> 2);
     int64_t gx;
     if (op.split_rows) {
       int i = tile_idx * 128 + (xr & 127);
@@ -100,27 +110,20 @@ __device__ __forceinline__ KcRows<WAVES> kc_rows(const Operand& op, int x0, int 
       gx = x0 + xr;
       if (gx >= op.rows) gx = op.rows - 1;
     }
-    r.off[j] = op.src.row_index(gx);
+    r.row[q] = op.src.row(gx);
   }
   return r;
 }
 
-template <int WAVES>
-__device__ __forceinline__ void copy_kc(uint8_t* lds, const Operand& op, const KcRows<WAVES>& rows, int k0, int K,
-                                        int wave, int lane) {
+// RAGGED: K may end inside the stage; the chunks past K copy the last whole
+// chunk instead (those fragments are zeroed before use).
+template <int WAVES, bool RAGGED>
+__device__ __forceinline__ void copy_kc(uint8_t* lds, const KcRows<WAVES>& rows, int k0, int K, int wave) {
+  int k = k0 + rows.c8;
+  if constexpr (RAGGED) k = min(k, K - 8);
 #pragma unroll
-  for (int q = 0; q < 16 / WAVES; ++q) {
-    const int kb = wave + WAVES * q;
-    const int kk = kb >> 3;
-    const int row = 32 * (kb & 7) + (lane >> 1);
-    const uint32_t o = rows.off[q % (8 / WAVES)];
-    const uint16_t* base = ((o & 0x80000000u) ? op.src.peer : op.src.own) +
-                           static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld;
-    const int hh = (lane & 1) ^ ((row >> 2) & 1);
-    int k = k0 + kk * 16 + hh * 8;
-    if (k >= K) k = K - 8;            // those fragments are zeroed before use
-    __builtin_amdgcn_global_load_lds(GPTR(base + k), LPTR(lds + kb * 1024), 16, 0, 0);
-  }
+  for (int q = 0; q < 16 / WAVES; ++q)
+    __builtin_amdgcn_global_load_lds(GPTR(rows.row[q] + k), LPTR(lds + (wave + WAVES * q) * 1024), 16, 0, 0);
 }
 
 template <int WAVES>
@@ -318,7 +321,7 @@ __device__ __forceinline__ int lo_col(int wn, int j) {
   }
 }
 
-// -------------------------------------------------------------- the kernel
+// -------------------------------------------------------------- the kernels
 
 // Workgroup barrier between pipeline steps.  __syncthreads() would also fence
 // global memory, i.e. wait for every copy still in flight -- including the
@@ -339,31 +342,73 @@ __device__ __forceinline__ void wait_vm() {
   else asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
 }
 
-template <Layout LA, Layout LB, EpiKind KIND, int PAIR, int WAVES>
-__global__ void __launch_bounds__(WAVES * 64, 1) gemm_kernel(GemmParams p) {
-  constexpr int NS = WAVES == 8 ? 2 : 4;     // 32-column blocks per wave (half of them low)
-  constexpr int PER = 16 / WAVES;           // copies per operand per stage per wave
-  __shared__ __attribute__((aligned(16))) uint8_t a0[TILE_BYTES], b0[TILE_BYTES], a1[TILE_BYTES], b1[TILE_BYTES];
-  __shared__ __attribute__((aligned(16))) uint8_t a2[TILE_BYTES], b2[TILE_BYTES], a3[TILE_BYTES], b3[TILE_BYTES];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// Epilogue: each wave stages R rows x (NS*32) columns of fp32 at a time in its
+// own 16 KB of LDS (column halves swapped on rows with bit 2 set, so the two
+// half-waves write different banks) and hands out 8-column vectors of its low
+// blocks with their PAIR partners.  Accumulator register i of a lane: row
+// 8(i/4) + 4(lane/32) + i%4, column lane%32 of its 32x32 tile.
+template <EpiKind KIND, int PAIR, int NS>
+__device__ __forceinline__ void store_tile(const GemmParams& p, f32x16 (&acc)[4][NS], float* st, int64_t row0,
+                                           int tn, const int* ncol, int lane) {
+  constexpr int C = NS * 32, R = 4096 / C, PASSES = 128 / R, MS_PER = R / 32;
+#pragma unroll
+  for (int pass = 0; pass < PASSES; ++pass) {
+#pragma unroll
+    for (int mm = 0; mm < MS_PER; ++mm)
+#pragma unroll
+      for (int ns = 0; ns < NS; ++ns)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = mm * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+          const int cc = (ns * 32 + (lane & 31)) ^ (((r >> 2) & 1) << 4);
+          st[r * C + cc] = acc[pass * MS_PER + mm][ns][i];
+        }
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+    constexpr int VEC = R * (NS / 2) * 4;  // 8-column vectors of the low blocks per pass
+#pragma unroll 1
+    for (int it = 0; it < VEC / 64; ++it) {
+      const int idx = it * 64 + lane;
+      const int rr = idx / ((NS / 2) * 4), v = idx % ((NS / 2) * 4);
+      const int j = v >> 2, c8 = (v & 3) * 8;
+      const int flip = ((rr >> 2) & 1) << 4;
+      const float4* lo4 = reinterpret_cast<const float4*>(st + rr * C + ((j * 32 + c8) ^ flip));
+      const float4* hi4 = reinterpret_cast<const float4*>(st + rr * C + (((j + NS / 2) * 32 + c8) ^ flip));
+      const float4 l0 = lo4[0], l1 = lo4[1], h0 = hi4[0], h1 = hi4[1];
+      float lo[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
+      float hi[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+      epilogue<KIND, PAIR>(p, row0 + pass * R + rr, tn, ncol[j] + c8, lo, hi);
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+  }
+}
 
+struct TileCoord {
+  int tm, tn;
+};
+__device__ __forceinline__ TileCoord tile_of(const GemmParams& p) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = p.B.split_rows ? (p.B.split_rows + 127) / 128 : (p.N + BN - 1) / BN;
   const int pid = xcd_remap(blockIdx.x, gridDim.x);
   const int group = GROUP_M * tiles_n;
   const int first_m = (pid / group) * GROUP_M;
   const int gm = min(tiles_m - first_m, GROUP_M);
-  const int tm = first_m + (pid % group) % gm;
-  const int tn = (pid % group) / gm;
-  const int m0 = tm * BM, n0 = tn * BN;
-  const int wm = WAVES == 8 ? (wave >> 2) : (wave >> 1);
-  const int wn = WAVES == 8 ? (wave & 3) : (wave & 1);
+  return TileCoord{first_m + (pid % group) % gm, (pid % group) / gm};
+}
+
+// 8 waves (two per SIMD), each 128 x 64.
+template <Layout LA, Layout LB, EpiKind KIND, int PAIR>
+__global__ void __launch_bounds__(512, 1) gemm_bk32(GemmParams p) {
+  constexpr int WAVES = 8, NS = 2, PER = 2;
+  constexpr bool RAGGED = true;
+  __shared__ __attribute__((aligned(16))) uint8_t a0[TILE_BYTES], b0[TILE_BYTES], a1[TILE_BYTES], b1[TILE_BYTES];
+  __shared__ __attribute__((aligned(16))) uint8_t a2[TILE_BYTES], b2[TILE_BYTES], a3[TILE_BYTES], b3[TILE_BYTES];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const TileCoord tc = tile_of(p);
+  const int tm = tc.tm, tn = tc.tn, m0 = tm * BM, n0 = tn * BN;
+  const int wm = wave >> 2, wn = wave & 3;
   int ncol[NS];
-#pragma unroll
-  for (int j = 0; j < NS / 2; ++j) {
-    ncol[j] = lo_col<WAVES, PAIR>(wn, j);
-    ncol[j + NS / 2] = ncol[j] + PAIR;
-  }
+  ncol[0] = lo_col<WAVES, PAIR>(wn, 0);
+  ncol[1] = ncol[0] + PAIR;
 
   f32x16 acc[4][NS];
 #pragma unroll
@@ -376,9 +421,9 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_kernel(GemmParams p) {
   if constexpr (LB == Layout::KC) rb = kc_rows<WAVES>(p.B, n0, tn, wave, lane);
 
   auto issue = [&](int k0, uint8_t* la, uint8_t* lb) {
-    if constexpr (LA == Layout::KC) copy_kc<WAVES>(la, p.A, ra, k0, p.K, wave, lane);
+    if constexpr (LA == Layout::KC) copy_kc<WAVES, RAGGED>(la, ra, k0, p.K, wave);
     else copy_mn<WAVES>(la, p.A, m0, k0, p.K, wave, lane);
-    if constexpr (LB == Layout::KC) copy_kc<WAVES>(lb, p.B, rb, k0, p.K, wave, lane);
+    if constexpr (LB == Layout::KC) copy_kc<WAVES, RAGGED>(lb, rb, k0, p.K, wave);
     else copy_mn<WAVES>(lb, p.B, n0, k0, p.K, wave, lane);
   };
   auto compute = [&](int k0, const uint8_t* la, const uint8_t* lb) {
@@ -437,87 +482,258 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_kernel(GemmParams p) {
   if (rest > 2) step(kt + 2, a2, b2, a1, b1);
   __syncthreads();   // every wave is done reading the stages before they become staging space
 
-  // Epilogue: each wave stages R rows x (NS*32) columns of fp32 at a time in
-  // its own 16 KB of LDS (column halves swapped on rows with bit 2 set, so the
-  // two half-waves write different banks) and hands out 8-column vectors of
-  // its low blocks with their PAIR partners.  Accumulator register i of a
-  // lane: row 8(i/4) + 4(lane/32) + i%4, column lane%32 of its 32x32 tile.
-  constexpr int C = NS * 32, R = 4096 / C, PASSES = 128 / R, MS_PER = R / 32;
-  const int sb = WAVES == 8 ? wave : 2 * wave;    // this wave's 16 KB staging buffer
-  uint8_t* mine = sb == 0 ? a0 : sb == 1 ? b0 : sb == 2 ? a1 : sb == 3 ? b1 : sb == 4 ? a2 : sb == 5 ? b2
-                : sb == 6 ? a3 : b3;
-  float* st = reinterpret_cast<float*>(mine);
-#pragma unroll
-  for (int pass = 0; pass < PASSES; ++pass) {
-#pragma unroll
-    for (int mm = 0; mm < MS_PER; ++mm)
-#pragma unroll
-      for (int ns = 0; ns < NS; ++ns)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int r = mm * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-          const int cc = (ns * 32 + (lane & 31)) ^ (((r >> 2) & 1) << 4);
-          st[r * C + cc] = acc[pass * MS_PER + mm][ns][i];
-        }
-    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-    constexpr int VEC = R * (NS / 2) * 4;  // 8-column vectors of the low blocks per pass
-#pragma unroll 1
-    for (int it = 0; it < VEC / 64; ++it) {
-      const int idx = it * 64 + lane;
-      const int rr = idx / ((NS / 2) * 4), v = idx % ((NS / 2) * 4);
-      const int j = v >> 2, c8 = (v & 3) * 8;
-      const int flip = ((rr >> 2) & 1) << 4;
-      const float4* lo4 = reinterpret_cast<const float4*>(st + rr * C + ((j * 32 + c8) ^ flip));
-      const float4* hi4 = reinterpret_cast<const float4*>(st + rr * C + (((j + NS / 2) * 32 + c8) ^ flip));
-      const float4 l0 = lo4[0], l1 = lo4[1], h0 = hi4[0], h1 = hi4[1];
-      float lo[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
-      float hi[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
-      const int64_t m = static_cast<int64_t>(m0) + wm * 128 + pass * R + rr;
-      epilogue<KIND, PAIR>(p, m, tn, ncol[j] + c8, lo, hi);
-    }
-    __builtin_amdgcn_s_waitcnt(0xc07f);
-  }
-  (void)n0;
+  uint8_t* mine = wave == 0 ? a0 : wave == 1 ? b0 : wave == 2 ? a1 : wave == 3 ? b1 : wave == 4 ? a2
+                : wave == 5 ? b2 : wave == 6 ? a3 : b3;
+  store_tile<KIND, PAIR, NS>(p, acc, reinterpret_cast<float*>(mine), static_cast<int64_t>(m0) + wm * 128, tn,
+                             ncol, lane);
 }
 
-int gemm_waves() {
-  static int w = [] {
-    const char* e = getenv("L4D_GEMM_WAVES");
-    return (e && atoi(e) == 4) ? 4 : 8;
+// ---------------------------------------------------------- BK = 64 variant
+// Two stages of 64 k (32 KB per operand each, 128 KB in all).  A KC copy
+// instruction moves 8 whole rows of 128 bytes (one cache line each, so no
+// line is fetched twice); an MN copy instruction moves 2 k-rows of 512 bytes.
+// KC slot s of row r holds chunk s ^ (r & 7): the 8 rows one 8-lane group of a
+// fragment read touches cover all 32 banks once.
+constexpr int BK2 = 64;
+constexpr int TILE2 = 256 * BK2 * 2;     // 32 KB per operand per stage
+
+__device__ __forceinline__ int kc2_off(int row, int chunk) { return row * 128 + ((chunk ^ (row & 7)) << 4); }
+
+template <int WAVES>
+struct Kc2Rows {
+  const uint16_t* row[32 / WAVES];
+  int c8;
+};
+
+template <int WAVES>
+__device__ __forceinline__ Kc2Rows<WAVES> kc2_rows(const Operand& op, int x0, int tile_idx, int wave, int lane) {
+  Kc2Rows<WAVES> r;
+  r.c8 = 8 * ((lane & 7) ^ ((lane >> 3) & 7));
+#pragma unroll
+  for (int q = 0; q < 32 / WAVES; ++q) {
+    const int xr = 8 * (wave + WAVES * q) + (lane >> 3);
+    int64_t gx;
+    if (op.split_rows) {
+      int i = tile_idx * 128 + (xr & 127);
+      if (i >= op.split_rows) i = op.split_rows - 1;
+      gx = (xr >= 128 ? op.split_off : 0) + i;
+    } else {
+      gx = x0 + xr;
+      if (gx >= op.rows) gx = op.rows - 1;
+    }
+    r.row[q] = op.src.row(gx);
+  }
+  return r;
+}
+
+template <int WAVES>
+__device__ __forceinline__ void copy2_kc(uint8_t* lds, const Kc2Rows<WAVES>& rows, int k0, int wave) {
+  const int k = k0 + rows.c8;
+#pragma unroll
+  for (int q = 0; q < 32 / WAVES; ++q)
+    __builtin_amdgcn_global_load_lds(GPTR(rows.row[q] + k), LPTR(lds + (wave + WAVES * q) * 1024), 16, 0, 0);
+}
+
+template <int WAVES>
+__device__ __forceinline__ void copy2_mn(uint8_t* lds, const Operand& op, int x0, int k0, int wave, int lane) {
+#pragma unroll
+  for (int q = 0; q < 32 / WAVES; ++q) {
+    const int kb = wave + WAVES * q;
+    const int kr = 2 * kb + (lane >> 5);
+    const int lc = (lane & 31) ^ mn_swz(kr);
+    int x = x0 + lc * 8;
+    if (x >= op.rows) x = op.rows - 8;
+    const uint32_t o = op.src.row_index(k0 + kr);
+    const uint16_t* base = (o & 0x80000000u) ? op.src.peer : op.src.own;
+    __builtin_amdgcn_global_load_lds(GPTR(base + static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld + x),
+                                     LPTR(lds + kb * 1024), 16, 0, 0);
+  }
+}
+
+template <int NS>
+struct Frags2 {
+  bf16x8 a[4], b[NS];
+};
+
+// KC fragment of rows x0 + lane%32 (x0 a multiple of 32), k = 16 kk + 8 (lane/32) + 0..7.
+template <Layout L>
+__device__ __forceinline__ bf16x8 frag2(const uint8_t* lds, int x0, int kk, int lane) {
+  if constexpr (L == Layout::KC) {
+    return *reinterpret_cast<const bf16x8*>(lds + kc2_off(x0 + (lane & 31), 2 * kk + (lane >> 5)));
+  } else {
+    return frag<Layout::MN>(lds, x0, kk, lane);
+  }
+}
+
+template <Layout LA, Layout LB, int NS>
+__device__ __forceinline__ void read_frags2(Frags2<NS>& f, const uint8_t* la, const uint8_t* lb, int wm,
+                                            const int* ncol, int kk, int lane) {
+#pragma unroll
+  for (int ms = 0; ms < 4; ++ms) f.a[ms] = frag2<LA>(la, wm * 128 + ms * 32, kk, lane);
+#pragma unroll
+  for (int ns = 0; ns < NS; ++ns) f.b[ns] = frag2<LB>(lb, ncol[ns], kk, lane);
+}
+
+template <int NS>
+__device__ __forceinline__ void mfma_frags2(f32x16 (&acc)[4][NS], const Frags2<NS>& f) {
+#pragma unroll
+  for (int ms = 0; ms < 4; ++ms)
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns)
+      acc[ms][ns] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[ms], f.b[ns], acc[ms][ns], 0, 0, 0);
+}
+
+// Spread DS reads over the MFMAs of a sub-step: 8 slots of (DS share, M MFMAs).
+template <int DS, int M, int I = 0>
+__device__ __forceinline__ void interleave2_slots() {
+  if constexpr (I < 8) {
+    constexpr int n = (DS * (I + 1)) / 8 - (DS * I) / 8;
+    if constexpr (n > 0) __builtin_amdgcn_sched_group_barrier(0x100, n, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, M, 0);
+    interleave2_slots<DS, M, I + 1>();
+  }
+}
+template <Layout LA, Layout LB, int NS>
+__device__ __forceinline__ void interleave2() {
+  interleave2_slots<4 * (LA == Layout::KC ? 1 : 2) + NS * (LB == Layout::KC ? 1 : 2), NS / 2>();
+}
+
+template <Layout LA, Layout LB, EpiKind KIND, int PAIR, int WAVES>
+__global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
+  constexpr int NS = WAVES == 8 ? 2 : 4;
+  constexpr int PER = 32 / WAVES;           // copy instructions per operand per stage per wave
+  __shared__ __attribute__((aligned(16))) uint8_t a0[TILE2], b0[TILE2], a1[TILE2], b1[TILE2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const TileCoord tc = tile_of(p);
+  const int tm = tc.tm, tn = tc.tn, m0 = tm * BM, n0 = tn * BN;
+  const int wm = WAVES == 8 ? (wave >> 2) : (wave >> 1);
+  const int wn = WAVES == 8 ? (wave & 3) : (wave & 1);
+  int ncol[NS];
+#pragma unroll
+  for (int j = 0; j < NS / 2; ++j) {
+    ncol[j] = lo_col<WAVES, PAIR>(wn, j);
+    ncol[j + NS / 2] = ncol[j] + PAIR;
+  }
+
+  f32x16 acc[4][NS];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
+
+  Kc2Rows<WAVES> ra{}, rb{};
+  if constexpr (LA == Layout::KC) ra = kc2_rows<WAVES>(p.A, m0, tm, wave, lane);
+  if constexpr (LB == Layout::KC) rb = kc2_rows<WAVES>(p.B, n0, tn, wave, lane);
+  auto issue = [&](int k0, uint8_t* la, uint8_t* lb) {
+    if constexpr (LA == Layout::KC) copy2_kc<WAVES>(la, ra, k0, wave);
+    else copy2_mn<WAVES>(la, p.A, m0, k0, wave, lane);
+    if constexpr (LB == Layout::KC) copy2_kc<WAVES>(lb, rb, k0, wave);
+    else copy2_mn<WAVES>(lb, p.B, n0, k0, wave, lane);
+  };
+
+  // K is a multiple of 2 * BK2 (the host picks this kernel only then).
+  const int nk = p.K / BK2;
+  Frags2<NS> f0, f1;
+  // Stage kt (buffers X, next stage in Y): sub-steps kk = 0..3 each read the
+  // fragments of the next sub-step under their own MFMAs.  Before the last
+  // sub-step every wave has read all of X: wait for stage kt+1, publish it
+  // with the barrier, refill X with stage kt+2 and read the first fragments
+  // of Y under the last MFMAs.
+  auto stage = [&](int kt, uint8_t* xa, uint8_t* xb, const uint8_t* ya, const uint8_t* yb) {
+    read_frags2<LA, LB, NS>(f1, xa, xb, wm, ncol, 1, lane);
+    mfma_frags2<NS>(acc, f0);
+    interleave2<LA, LB, NS>();
+    read_frags2<LA, LB, NS>(f0, xa, xb, wm, ncol, 2, lane);
+    mfma_frags2<NS>(acc, f1);
+    interleave2<LA, LB, NS>();
+    read_frags2<LA, LB, NS>(f1, xa, xb, wm, ncol, 3, lane);
+    mfma_frags2<NS>(acc, f0);
+    interleave2<LA, LB, NS>();
+    wait_vm<0>();
+    stage_barrier();
+    issue(min(kt + 2, nk - 1) * BK2, xa, xb);
+    read_frags2<LA, LB, NS>(f0, ya, yb, wm, ncol, 0, lane);   // after the last stage: read, never used
+    mfma_frags2<NS>(acc, f1);
+    interleave2<LA, LB, NS>();
+  };
+
+  issue(0, a0, b0);
+  issue(BK2, a1, b1);
+  if constexpr (PER == 8) wait_vm<16>();
+  else wait_vm<8>();
+  stage_barrier();
+  read_frags2<LA, LB, NS>(f0, a0, b0, wm, ncol, 0, lane);
+  for (int kt = 0; kt < nk; kt += 2) {
+    stage(kt, a0, b0, a1, b1);
+    stage(kt + 1, a1, b1, a0, b0);
+  }
+  __syncthreads();   // every copy has landed and every wave is done reading the stages
+
+  uint8_t* mine = (WAVES == 8 ? (wave >> 1) : wave) == 0 ? a0
+                : (WAVES == 8 ? (wave >> 1) : wave) == 1 ? b0
+                : (WAVES == 8 ? (wave >> 1) : wave) == 2 ? a1 : b1;
+  if constexpr (WAVES == 8) mine += (wave & 1) * 16384;
+  store_tile<KIND, PAIR, NS>(p, acc, reinterpret_cast<float*>(mine), static_cast<int64_t>(m0) + wm * 128, tn,
+                             ncol, lane);
+}
+
+// Kernel choice: K a multiple of 128 takes the 8-wave BK = 64 kernel (the
+// fastest of the three on the Llama layer shapes), any other K the BK = 32
+// kernel.  L4D_GEMM_VARIANT = 32 | 64 (4-wave BK = 64) | 68 forces one.
+int gemm_variant_env() {
+  static int v = [] {
+    const char* e = getenv("L4D_GEMM_VARIANT");
+    return e ? atoi(e) : 0;
   }();
-  return w;
+  return v;
 }
 
 template <Layout LA, Layout LB, EpiKind KIND, int PAIR>
-hipError_t launch(const GemmParams& p, hipStream_t stream) {
+hipError_t launch(const GemmParams& p, hipStream_t stream, int variant) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = p.B.split_rows ? (p.B.split_rows + 127) / 128 : (p.N + BN - 1) / BN;
-  if (gemm_waves() == 4)
-    hipLaunchKernelGGL((gemm_kernel<LA, LB, KIND, PAIR, 4>), dim3(tiles_m * tiles_n), dim3(256), 0, stream, p);
+  const dim3 grid(tiles_m * tiles_n);
+  if (variant == 0) variant = gemm_variant_env();
+  if (variant == 0) variant = 68;
+  if (p.K % (2 * BK2) != 0) variant = 32;
+  if constexpr (LA == Layout::MN) {
+    if (variant == 64) variant = 68;     // the 4-wave kernel needs stack space with two MN operands
+  }
+  if (variant == 64) {
+    if constexpr (LA != Layout::MN)
+      hipLaunchKernelGGL((gemm_bk64<LA, LB, KIND, PAIR, 4>), grid, dim3(256), 0, stream, p);
+  } else if (variant == 68)
+    hipLaunchKernelGGL((gemm_bk64<LA, LB, KIND, PAIR, 8>), grid, dim3(512), 0, stream, p);
   else
-    hipLaunchKernelGGL((gemm_kernel<LA, LB, KIND, PAIR, 8>), dim3(tiles_m * tiles_n), dim3(512), 0, stream, p);
+    hipLaunchKernelGGL((gemm_bk32<LA, LB, KIND, PAIR>), grid, dim3(512), 0, stream, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
+hipError_t gemm_variant(const GemmParams& p, Layout la, Layout lb, hipStream_t stream, int variant);
+
 hipError_t gemm(const GemmParams& p, Layout la, Layout lb, hipStream_t stream) {
+  return gemm_variant(p, la, lb, stream, 0);
+}
+
+hipError_t gemm_variant(const GemmParams& p, Layout la, Layout lb, hipStream_t stream, int variant) {
   if (p.M <= 0 || p.N <= 0 || p.K <= 0) return hipSuccess;
   using L = Layout;
   using E = EpiKind;
   const E k = p.epi.kind;
   if (la == L::KC && lb == L::KC) {
-    if (k == E::QkvRope && p.epi.d_h == 128) return launch<L::KC, L::KC, E::QkvRope, 64>(p, stream);
-    if (k == E::QkvRope && p.epi.d_h == 64) return launch<L::KC, L::KC, E::QkvRope, 32>(p, stream);
-    if (k == E::ResidualSP) return launch<L::KC, L::KC, E::ResidualSP, 128>(p, stream);
-    if (k == E::SwiGLUFwd) return launch<L::KC, L::KC, E::SwiGLUFwd, 128>(p, stream);
-    if (k == E::StoreBF16) return launch<L::KC, L::KC, E::StoreBF16, 128>(p, stream);
+    if (k == E::QkvRope && p.epi.d_h == 128) return launch<L::KC, L::KC, E::QkvRope, 64>(p, stream, variant);
+    if (k == E::QkvRope && p.epi.d_h == 64) return launch<L::KC, L::KC, E::QkvRope, 32>(p, stream, variant);
+    if (k == E::ResidualSP) return launch<L::KC, L::KC, E::ResidualSP, 128>(p, stream, variant);
+    if (k == E::SwiGLUFwd) return launch<L::KC, L::KC, E::SwiGLUFwd, 128>(p, stream, variant);
+    if (k == E::StoreBF16) return launch<L::KC, L::KC, E::StoreBF16, 128>(p, stream, variant);
   } else if (la == L::KC && lb == L::MN) {
-    if (k == E::SwiGLUBwd) return launch<L::KC, L::MN, E::SwiGLUBwd, 128>(p, stream);
-    if (k == E::ResidualSP) return launch<L::KC, L::MN, E::ResidualSP, 128>(p, stream);
-    if (k == E::StoreBF16) return launch<L::KC, L::MN, E::StoreBF16, 128>(p, stream);
+    if (k == E::SwiGLUBwd) return launch<L::KC, L::MN, E::SwiGLUBwd, 128>(p, stream, variant);
+    if (k == E::ResidualSP) return launch<L::KC, L::MN, E::ResidualSP, 128>(p, stream, variant);
+    if (k == E::StoreBF16) return launch<L::KC, L::MN, E::StoreBF16, 128>(p, stream, variant);
   } else if (la == L::MN && lb == L::MN) {
-    if (k == E::AccF32) return launch<L::MN, L::MN, E::AccF32, 128>(p, stream);
+    if (k == E::AccF32) return launch<L::MN, L::MN, E::AccF32, 128>(p, stream, variant);
   }
   return hipErrorInvalidValue;     // a layout / epilogue pairing the layer never uses
 }
