@@ -27,6 +27,8 @@
 //    result is deterministic.
 #include <math.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace l4d {
@@ -44,7 +46,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int KT = 64;            // keys per tile (forward, dQ)
-constexpr int QT = 32;            // queries per tile (dK/dV)
+constexpr int QT = 64;            // queries per tile (dK/dV)
 
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
@@ -57,7 +59,16 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
-__device__ __forceinline__ void wait_tiles() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most N of this wave's copies are still in flight.
+template <int N>
+__device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+// Workgroup barrier that does not drain the copies still in flight (unlike
+// __syncthreads): only this wave's LDS reads must be done before it.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 // ------------------------------------------------------------------ LDS tiles
 // Row-major [rows][D] bf16 tile; 16-byte chunk c of row r sits at chunk c ^ swz(r).
@@ -121,9 +132,13 @@ __device__ __forceinline__ bf16x8 frag_acc(const f32x16& s, int i0) {
 // Row of accumulator register i for this lane (32x32 MFMA output layout).
 __device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 
+// Global position of local query row `row` (at most two chunks).  A select
+// between the two scalar chunk ids, not an indexed load: a per-lane index into
+// the kernel arguments would become a vector load whose wait drains every copy
+// in flight.
 __device__ __forceinline__ int qpos(const ChunkMap& m, int row) {
-  const int c = row / m.chunk_len;
-  return m.chunk_id[c] * m.chunk_len + (row - c * m.chunk_len);
+  const bool second = row >= m.chunk_len;
+  return (second ? m.chunk_id[1] : m.chunk_id[0]) * m.chunk_len + (second ? row - m.chunk_len : row);
 }
 
 // Key tile `tile` (of `tsz` tokens) across the segments.
@@ -155,12 +170,50 @@ __device__ __forceinline__ int next_key_tile(const AttnParams& p, int from, int 
   return ntiles;
 }
 
+
+// Three-stage copy ring over a sequence of work items (key or query tiles):
+// item k lives in buffer k % 3; while item k is computed the copies of items
+// k+1 and k+2 are in flight.  `next(i)` is the first wanted item at or after
+// i (`total` when none), `issue(item, buffer)` starts its copies (NC
+// instructions per wave, the same count for every item) and
+// `compute(item, buffer)` uses it.  Buffer b is passed as the constant
+// std::integral_constant<int, b>, so every LDS object is named statically and
+// the compiler sees that the reads of one buffer do not depend on the copies
+// landing in the others.
+template <int NC, class Next, class Issue, class Compute>
+__device__ __forceinline__ void run_ring(int total, Next next, Issue issue, Compute compute) {
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using B2 = std::integral_constant<int, 2>;
+  int c0 = next(0);
+  int c1 = c0 < total ? next(c0 + 1) : total;
+  if (c0 < total) issue(c0, B0{});
+  if (c1 < total) issue(c1, B1{});
+  auto step = [&](auto cur_buf, auto far_buf) __attribute__((always_inline)) {
+    if (c1 < total) wait_copies<NC>();     // item c0 has landed; c1 may still be in flight
+    else wait_copies<0>();
+    ring_barrier();                        // every wave's copy of c0 is visible; the buffer of c0-1 is free
+    const int c2 = c1 < total ? next(c1 + 1) : total;
+    if (c2 < total) issue(c2, far_buf);
+    compute(c0, cur_buf);
+    c0 = c1;
+    c1 = c2;
+  };
+  while (c0 < total) {
+    step(B0{}, B2{});
+    if (c0 >= total) break;
+    step(B1{}, B0{});
+    if (c0 >= total) break;
+    step(B2{}, B1{});
+  }
+}
+
 // ------------------------------------------------------------------ forward
 // grid: (q tiles of 128, a_t heads, b); 4 waves x 32 queries.
 template <int D>
-__global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
+__global__ void __launch_bounds__(256, 1) attn_fwd_kernel(AttnParams p) {
   constexpr int TB = KT * D * 2;
-  __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB];
+  __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB], k2[TB], v2[TB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n_qt = (p.n_q + 127) / 128;
   const int qt = n_qt - 1 - blockIdx.x;         // heaviest tiles first
@@ -187,13 +240,13 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
   for (int i = 0; i < D / 32; ++i) o[i] = f32x16{};
 
   const int ntiles = total_tiles(p, KT);
-  auto issue = [&](int seg, int t0, uint8_t* kt, uint8_t* vt) {
+  auto issue = [&](int seg, int t0, uint8_t* kt, uint8_t* vt) __attribute__((always_inline)) {
     const KvSeg& s = p.seg[seg];
     const int64_t off = bi * s.bstride + static_cast<int64_t>(t0) * s.ld + hk * D;
     tile_load<D, KT>(kt, s.k + off, s.ld, s.n - t0, wave, lane);
     tile_load<D, KT>(vt, s.v + off, s.ld, s.n - t0, wave, lane);
   };
-  auto compute = [&](int seg, int t0, const uint8_t* kt, const uint8_t* vt) {
+  auto compute = [&](int seg, int t0, const uint8_t* kt, const uint8_t* vt) __attribute__((always_inline)) {
     const KvSeg& s = p.seg[seg];
     const int kpos0 = s.pos0 + t0;
     const int kvalid = min(KT, s.n - t0);
@@ -244,30 +297,32 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
       }
   };
 
-  int seg, t0, nseg, nt0;
-  int cur = next_key_tile(p, 0, ntiles, pos_max, seg, t0);
-  if (cur < ntiles) issue(seg, t0, k0, v0);
-  wait_tiles();
-  __syncthreads();
-  while (cur < ntiles) {
-    int nxt = next_key_tile(p, cur + 1, ntiles, pos_max, nseg, nt0);
-    if (nxt < ntiles) issue(nseg, nt0, k1, v1);
-    compute(seg, t0, k0, v0);
-    wait_tiles();
-    __syncthreads();
-    cur = nxt;
-    seg = nseg;
-    t0 = nt0;
-    if (cur >= ntiles) break;
-    nxt = next_key_tile(p, cur + 1, ntiles, pos_max, nseg, nt0);
-    if (nxt < ntiles) issue(nseg, nt0, k0, v0);
-    compute(seg, t0, k1, v1);
-    wait_tiles();
-    __syncthreads();
-    cur = nxt;
-    seg = nseg;
-    t0 = nt0;
-  }
+  auto kbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
+    if constexpr (decltype(b)::value == 0) return k0;
+    else if constexpr (decltype(b)::value == 1) return k1;
+    else return k2;
+  };
+  auto vbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
+    if constexpr (decltype(b)::value == 0) return v0;
+    else if constexpr (decltype(b)::value == 1) return v1;
+    else return v2;
+  };
+  run_ring<KT * D / 1024>(
+      ntiles,
+      [&](int from) __attribute__((always_inline)) {
+        int s_, t_;
+        return next_key_tile(p, from, ntiles, pos_max, s_, t_);
+      },
+      [&](int t, auto b) __attribute__((always_inline)) {
+        int s_, t_;
+        find_tile(p, t, KT, s_, t_);
+        issue(s_, t_, kbuf(b), vbuf(b));
+      },
+      [&](int t, auto b) __attribute__((always_inline)) {
+        int s_, t_;
+        find_tile(p, t, KT, s_, t_);
+        compute(s_, t_, kbuf(b), vbuf(b));
+      });
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (!q_ok) return;
@@ -318,8 +373,8 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(AttnParams p) {
 template <int D>
 __global__ void __launch_bounds__(256, 1) attn_bwd_dkdv_kernel(AttnParams p) {
   constexpr int TB = QT * D * 2;
-  __shared__ __attribute__((aligned(16))) uint8_t q0[TB], g0[TB], q1[TB], g1[TB];   // Q and dO tiles
-  __shared__ __attribute__((aligned(16))) float st0[2][QT], st1[2][QT];             // lse*log2e, delta
+  __shared__ __attribute__((aligned(16))) uint8_t q0[TB], g0[TB], q1[TB], g1[TB], q2[TB], g2[TB];   // Q, dO tiles
+  __shared__ __attribute__((aligned(16))) float st0[2][QT], st1[2][QT], st2[2][QT];                  // lse, delta
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int group = p.a_t / p.k_t;
   const int hpb = group / p.n_split;
@@ -355,7 +410,7 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkdv_kernel(AttnParams p) {
   const int n_qt = (p.n_q + QT - 1) / QT;
   const int total = hpb * n_qt;
   const int head0 = hk * group + split * hpb;
-  auto next_wanted = [&](int from) {
+  auto next_wanted = [&](int from) __attribute__((always_inline)) {
     for (int it = from; it < total; ++it) {
       const int qt = it % n_qt;
       const int last = min(qt * QT + QT - 1, p.n_q - 1);
@@ -363,54 +418,61 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkdv_kernel(AttnParams p) {
     }
     return total;
   };
-  auto issue = [&](int it, uint8_t* qt_l, uint8_t* gt_l, float (*st)[QT]) {
+  auto issue = [&](int it, uint8_t* qt_l, uint8_t* gt_l, float (*st)[QT]) __attribute__((always_inline)) {
     const int hq = head0 + it / n_qt, qt = it % n_qt;
-    if (tid < QT) {     // before the tile copies, so its wait does not cover them
-      const int q = qt * QT + tid;
-      const int64_t idx = (static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + (q < p.n_q ? q : 0);
-      st[0][tid] = q < p.n_q ? p.lse[idx] * kLog2e : INFINITY;
-      st[1][tid] = q < p.n_q ? p.delta[idx] : 0.f;
+    if (lane < 16) {    // wave w copies the statistics of queries 16w .. 16w+15 (rows past n_q: the last row)
+      const int q = min(qt * QT + wave * 16 + lane, p.n_q - 1);
+      const int64_t idx = (static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + q;
+      __builtin_amdgcn_global_load_lds(GPTR(p.lse + idx), LPTR(&st[0][wave * 16]), 4, 0, 0);
+      __builtin_amdgcn_global_load_lds(GPTR(p.delta + idx), LPTR(&st[1][wave * 16]), 4, 0, 0);
     }
     const int64_t off = bi * p.q_bstride + static_cast<int64_t>(qt * QT) * p.q_ld + hq * D;
     tile_load<D, QT>(qt_l, p.q + off, p.q_ld, p.n_q - qt * QT, wave, lane);
     tile_load<D, QT>(gt_l, p.dout + off, p.q_ld, p.n_q - qt * QT, wave, lane);
   };
-  auto compute = [&](int it, const uint8_t* qt_l, const uint8_t* gt_l, const float (*st)[QT]) {
+  // One query tile: the wave's 32 keys against 64 queries as two 32-query
+  // halves, so S^T and dP^T run as four independent MFMA chains.
+  auto compute = [&](int it, const uint8_t* qt_l, const uint8_t* gt_l, const float (*st)[QT]) __attribute__((always_inline)) {
     const int qt = it % n_qt;
     const int qr0 = qt * QT;
     const int qlast = min(qr0 + QT - 1, p.n_q - 1);
     const int qp0 = qpos(p.qmap, qr0), qpl = qpos(p.qmap, qlast);
     if (qpl < wave_kpos0) return;                        // every query of the tile precedes this wave's keys
-    f32x16 sc = f32x16{}, dp = f32x16{};
+    f32x16 sc[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-      sc = mfma(frag_rows<D>(qt_l, 0, kk, lane), kf[kk], sc);
-      dp = mfma(frag_rows<D>(gt_l, 0, kk, lane), vf[kk], dp);
-    }
+    for (int kk = 0; kk < D / 16; ++kk)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        sc[h] = mfma(frag_rows<D>(qt_l, 32 * h, kk, lane), kf[kk], sc[h]);
+        dp[h] = mfma(frag_rows<D>(gt_l, 32 * h, kk, lane), vf[kk], dp[h]);
+      }
     const bool full = qp0 >= wave_kpos0 + 31 && qlast == qr0 + QT - 1 && qpl - qp0 == QT - 1;
     const bool contiguous = qpl - qp0 == qlast - qr0;
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      const float4 ls = *reinterpret_cast<const float4*>(&st[0][8 * jj + rbase]);
-      const float4 de = *reinterpret_cast<const float4*>(&st[1][8 * jj + rbase]);
-      const float lsv[4] = {ls.x, ls.y, ls.z, ls.w}, dev[4] = {de.x, de.y, de.z, de.w};
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int i = 4 * jj + u;
-        float pr = fast_exp2(fmaf(sc[i], c, -lsv[u]));
-        if (!full) {
-          const int qr = 8 * jj + rbase + u;
-          const int qp = contiguous ? qp0 + qr : (qr0 + qr <= qlast ? qpos(p.qmap, qr0 + qr) : -1);
-          if (qr0 + qr > qlast || my_kpos > qp || !key_ok) pr = 0.f;
+      for (int jj = 0; jj < 4; ++jj) {
+        const float4 ls = *reinterpret_cast<const float4*>(&st[0][32 * h + 8 * jj + rbase]);
+        const float4 de = *reinterpret_cast<const float4*>(&st[1][32 * h + 8 * jj + rbase]);
+        const float lsv[4] = {ls.x * kLog2e, ls.y * kLog2e, ls.z * kLog2e, ls.w * kLog2e};
+        const float dev[4] = {de.x, de.y, de.z, de.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int i = 4 * jj + u;
+          float pr = fast_exp2(fmaf(sc[h][i], c, -lsv[u]));
+          if (!full) {
+            const int qr = 32 * h + 8 * jj + rbase + u;
+            const int qp = contiguous ? qp0 + qr : (qr0 + qr <= qlast ? qpos(p.qmap, qr0 + qr) : -1);
+            if (qr0 + qr > qlast || my_kpos > qp || !key_ok) pr = 0.f;
+          }
+          sc[h][i] = pr;
+          dp[h][i] = pr * (dp[h][i] - dev[u]);
         }
-        sc[i] = pr;
-        dp[i] = pr * (dp[i] - dev[u]);
       }
-    }
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      const bf16x8 pf = frag_acc(sc, 8 * g);
-      const bf16x8 sf = frag_acc(dp, 8 * g);
+    for (int g = 0; g < 4; ++g) {                        // 16-query groups
+      const bf16x8 pf = frag_acc(sc[g >> 1], 8 * (g & 1));
+      const bf16x8 sf = frag_acc(dp[g >> 1], 8 * (g & 1));
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
         dv[dt] = mfma(frag_cols<D>(gt_l, dt, g, lane), pf, dv[dt]);
@@ -419,25 +481,24 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkdv_kernel(AttnParams p) {
     }
   };
 
-  int cur = next_wanted(0);
-  if (cur < total) issue(cur, q0, g0, st0);
-  wait_tiles();
-  __syncthreads();
-  while (cur < total) {
-    int nxt = next_wanted(cur + 1);
-    if (nxt < total) issue(nxt, q1, g1, st1);
-    compute(cur, q0, g0, st0);
-    wait_tiles();
-    __syncthreads();
-    cur = nxt;
-    if (cur >= total) break;
-    nxt = next_wanted(cur + 1);
-    if (nxt < total) issue(nxt, q0, g0, st0);
-    compute(cur, q1, g1, st1);
-    wait_tiles();
-    __syncthreads();
-    cur = nxt;
-  }
+  auto qbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
+    if constexpr (decltype(b)::value == 0) return q0;
+    else if constexpr (decltype(b)::value == 1) return q1;
+    else return q2;
+  };
+  auto gbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
+    if constexpr (decltype(b)::value == 0) return g0;
+    else if constexpr (decltype(b)::value == 1) return g1;
+    else return g2;
+  };
+  auto sbuf = [&](auto b) __attribute__((always_inline)) -> float (*)[QT] {
+    if constexpr (decltype(b)::value == 0) return st0;
+    else if constexpr (decltype(b)::value == 1) return st1;
+    else return st2;
+  };
+  run_ring<QT * D / 1024 + 2>(     // Q and dO tiles (QT * D * 2 bytes each over 4 waves), lse, delta
+      total, next_wanted, [&](int it, auto b) __attribute__((always_inline)) { issue(it, qbuf(b), gbuf(b), sbuf(b)); },
+      [&](int it, auto b) __attribute__((always_inline)) { compute(it, qbuf(b), gbuf(b), sbuf(b)); });
 
   if (!key_ok) return;
   // lane owns key my_key; register i of tile dt is d = 32 dt + acc_row(i)
@@ -553,7 +614,7 @@ __global__ void __launch_bounds__(64) attn_dkv_reduce_kernel(AttnParams p) {
 template <int D>
 __global__ void __launch_bounds__(256, 1) attn_bwd_dq_kernel(AttnParams p) {
   constexpr int TB = KT * D * 2;
-  __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB];
+  __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB], k2[TB], v2[TB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n_qt = (p.n_q + 127) / 128;
   const int qt = n_qt - 1 - blockIdx.x;
@@ -586,13 +647,13 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dq_kernel(AttnParams p) {
   for (int i = 0; i < D / 32; ++i) dq[i] = f32x16{};
 
   const int ntiles = total_tiles(p, KT);
-  auto issue = [&](int seg, int t0, uint8_t* kt, uint8_t* vt) {
+  auto issue = [&](int seg, int t0, uint8_t* kt, uint8_t* vt) __attribute__((always_inline)) {
     const KvSeg& s = p.seg[seg];
     const int64_t off = bi * s.bstride + static_cast<int64_t>(t0) * s.ld + hk * D;
     tile_load<D, KT>(kt, s.k + off, s.ld, s.n - t0, wave, lane);
     tile_load<D, KT>(vt, s.v + off, s.ld, s.n - t0, wave, lane);
   };
-  auto compute = [&](int seg, int t0, const uint8_t* kt, const uint8_t* vt) {
+  auto compute = [&](int seg, int t0, const uint8_t* kt, const uint8_t* vt) __attribute__((always_inline)) {
     const KvSeg& s = p.seg[seg];
     const int kpos0 = s.pos0 + t0;
     const int kvalid = min(KT, s.n - t0);
@@ -624,30 +685,33 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dq_kernel(AttnParams p) {
       }
   };
 
-  int seg, t0, nseg, nt0;
-  int cur = next_key_tile(p, 0, ntiles, pos_max, seg, t0);
-  if (cur < ntiles) issue(seg, t0, k0, v0);
-  wait_tiles();
-  __syncthreads();
-  while (cur < ntiles) {
-    int nxt = next_key_tile(p, cur + 1, ntiles, pos_max, nseg, nt0);
-    if (nxt < ntiles) issue(nseg, nt0, k1, v1);
-    compute(seg, t0, k0, v0);
-    wait_tiles();
-    __syncthreads();
-    cur = nxt;
-    seg = nseg;
-    t0 = nt0;
-    if (cur >= ntiles) break;
-    nxt = next_key_tile(p, cur + 1, ntiles, pos_max, nseg, nt0);
-    if (nxt < ntiles) issue(nseg, nt0, k0, v0);
-    compute(seg, t0, k1, v1);
-    wait_tiles();
-    __syncthreads();
-    cur = nxt;
-    seg = nseg;
-    t0 = nt0;
-  }
+  auto kbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
+    if constexpr (decltype(b)::value == 0) return k0;
+    else if constexpr (decltype(b)::value == 1) return k1;
+    else return k2;
+  };
+  auto vbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
+    if constexpr (decltype(b)::value == 0) return v0;
+    else if constexpr (decltype(b)::value == 1) return v1;
+    else return v2;
+  };
+  run_ring<KT * D / 1024>(
+      ntiles,
+      [&](int from) __attribute__((always_inline)) {
+        int s_, t_;
+        return next_key_tile(p, from, ntiles, pos_max, s_, t_);
+      },
+      [&](int t, auto b) __attribute__((always_inline)) {
+        int s_, t_;
+        find_tile(p, t, KT, s_, t_);
+        issue(s_, t_, kbuf(b), vbuf(b));
+      },
+      [&](int t, auto b) __attribute__((always_inline)) {
+        int s_, t_;
+        find_tile(p, t, KT, s_, t_);
+        compute(s_, t_, kbuf(b), vbuf(b));
+      });
+
   if (!q_ok) return;
   constexpr int HALF_T = D / 64;
   const float2* tab = p.rope + static_cast<int64_t>(my_q) * (D / 2);
