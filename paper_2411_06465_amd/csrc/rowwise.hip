@@ -79,37 +79,48 @@ __global__ void __launch_bounds__(256) rmsnorm_fwd_kernel(const uint16_t* __rest
   }
 }
 
-// Grid-stride over rows; each block keeps per-column partial sums of dy*xhat
-// and writes them to partial[blockIdx.x][h].
+// Grid-stride over rows, one 256-thread block per row: thread t owns the
+// 16-byte chunks t + 256 it (it < CPT, h <= 2048 * CPT) of every row, so it
+// keeps its columns' partial sums of dy*xhat in registers and writes them to
+// partial[blockIdx.x][h] at the end.  The two row sums go through LDS,
+// double-buffered by row parity so one barrier per row suffices.
+template <int CPT>
 __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ gain, const uint16_t* __restrict__ dy,
     const uint16_t* __restrict__ dres, uint16_t* __restrict__ dx, float* __restrict__ partial,
     int64_t rows, int32_t h, float eps) {
-  __shared__ float red[4][8192 / 4];   // per-wave partials, reduced in two halves
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ float sums[2][4][2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nch = h / 8;
-  float acc[kMaxChunks][8];
+  float acc[CPT][8];
 #pragma unroll
-  for (int it = 0; it < kMaxChunks; ++it)
+  for (int it = 0; it < CPT; ++it)
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[it][j] = 0.f;
   const u32x4* gr = reinterpret_cast<const u32x4*>(gain);
-  for (int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wave; row < rows;
-       row += static_cast<int64_t>(gridDim.x) * 4) {
+  int parity = 0;
+  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x, parity ^= 1) {
     const u32x4* xr = reinterpret_cast<const u32x4*>(x + row * h);
     const u32x4* dr = reinterpret_cast<const u32x4*>(dy + row * h);
-    u32x4 xv[kMaxChunks], dv[kMaxChunks];
-    float ss = 0.f, dot = 0.f;
+    u32x4 xv[CPT], dv[CPT], gv[CPT];
 #pragma unroll
-    for (int it = 0; it < kMaxChunks; ++it) {
-      const int c = lane + 64 * it;
+    for (int it = 0; it < CPT; ++it) {
+      const int c = tid + 256 * it;
       if (c < nch) {
         xv[it] = xr[c];
         dv[it] = dr[c];
+        gv[it] = gr[c];
+      }
+    }
+    float ss = 0.f, dot = 0.f;
+#pragma unroll
+    for (int it = 0; it < CPT; ++it) {
+      const int c = tid + 256 * it;
+      if (c < nch) {
         float f[8], d[8], g[8];
         unpack8(xv[it], f);
         unpack8(dv[it], d);
-        unpack8(gr[c], g);
+        unpack8(gv[it], g);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           ss += f[j] * f[j];
@@ -117,59 +128,83 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
         }
       }
     }
-    const float rstd = rsqrtf(wave_sum(ss) / h + eps);
-    // mean over the row of (gain*dy) * xhat
-    const float c_mean = wave_sum(dot) * rstd / h;
+    ss = wave_sum(ss);
+    dot = wave_sum(dot);
+    if (lane == 0) {
+      sums[parity][wave][0] = ss;
+      sums[parity][wave][1] = dot;
+    }
+    __syncthreads();
+    ss = (sums[parity][0][0] + sums[parity][1][0]) + (sums[parity][2][0] + sums[parity][3][0]);
+    dot = (sums[parity][0][1] + sums[parity][1][1]) + (sums[parity][2][1] + sums[parity][3][1]);
+    const float rstd = rsqrtf(ss / h + eps);
+    const float c_mean = dot * rstd / h;        // mean over the row of (gain*dy) * xhat
     const u32x4* rr = dres ? reinterpret_cast<const u32x4*>(dres + row * h) : nullptr;
     u32x4* out = reinterpret_cast<u32x4*>(dx + row * h);
 #pragma unroll
-    for (int it = 0; it < kMaxChunks; ++it) {
-      const int c = lane + 64 * it;
+    for (int it = 0; it < CPT; ++it) {
+      const int c = tid + 256 * it;
       if (c < nch) {
         float f[8], d[8], g[8], r[8];
         unpack8(xv[it], f);
         unpack8(dv[it], d);
-        unpack8(gr[c], g);
+        unpack8(gv[it], g);
         if (rr) unpack8(rr[c], r);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const float xh = f[j] * rstd;
           acc[it][j] += d[j] * xh;
-          float v = rstd * (g[j] * d[j] - xh * c_mean);
+          const float v = rstd * (g[j] * d[j] - xh * c_mean);
           r[j] = rr ? r[j] + v : v;
         }
         out[c] = pack8(r);
       }
     }
   }
-  // block reduction of acc over the 4 waves, in chunks of h/4 columns
-  for (int part = 0; part < 4; ++part) {
-    const int lo = part * (h / 4), hi = lo + h / 4;
+  float* pr = partial + static_cast<int64_t>(blockIdx.x) * h;
 #pragma unroll
-    for (int it = 0; it < kMaxChunks; ++it) {
-      const int c = lane + 64 * it;
-      if (c < nch) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int col = c * 8 + j;
-          if (col >= lo && col < hi) red[wave][col - lo] = acc[it][j];
-        }
-      }
+  for (int it = 0; it < CPT; ++it) {
+    const int c = tid + 256 * it;
+    if (c < nch) {
+      reinterpret_cast<float4*>(pr + c * 8)[0] = make_float4(acc[it][0], acc[it][1], acc[it][2], acc[it][3]);
+      reinterpret_cast<float4*>(pr + c * 8)[1] = make_float4(acc[it][4], acc[it][5], acc[it][6], acc[it][7]);
     }
-    __syncthreads();
-    for (int col = threadIdx.x; col < h / 4; col += 256)
-      partial[static_cast<int64_t>(blockIdx.x) * h + lo + col] =
-          red[0][col] + red[1][col] + red[2][col] + red[3][col];
-    __syncthreads();
   }
 }
 
-__global__ void reduce_rows_add_kernel(const float* __restrict__ partial, int32_t n_partial, int32_t h,
-                                       float* __restrict__ out) {
-  const int col = blockIdx.x * blockDim.x + threadIdx.x;
+// Column sums of partial[n][h] in two deterministic levels (no atomics):
+// level 1 sums each slice of 64 rows into the slice's first row, in place,
+// a block per (64 columns, slice) with its 4 waves taking every 4th row;
+// level 2 adds the slice sums, in slice order, into out.
+__global__ void __launch_bounds__(256) reduce_slices_kernel(float* __restrict__ partial, int32_t n, int32_t h) {
+  __shared__ float s4[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = blockIdx.x * 64 + lane;
+  const int r0 = blockIdx.y * 64, r1 = min(r0 + 64, n);
+  float s = 0.f;
+  if (col < h) {
+    int i = r0 + wave;
+    for (; i + 12 < r1; i += 16) {     // four independent loads in flight
+      const float a = partial[static_cast<int64_t>(i) * h + col];
+      const float b = partial[static_cast<int64_t>(i + 4) * h + col];
+      const float c = partial[static_cast<int64_t>(i + 8) * h + col];
+      const float d = partial[static_cast<int64_t>(i + 12) * h + col];
+      s += (a + b) + (c + d);
+    }
+    for (; i < r1; i += 4) s += partial[static_cast<int64_t>(i) * h + col];
+  }
+  s4[wave][lane] = s;
+  __syncthreads();
+  if (wave == 0 && col < h)
+    partial[static_cast<int64_t>(r0) * h + col] = (s4[0][lane] + s4[1][lane]) + (s4[2][lane] + s4[3][lane]);
+}
+
+__global__ void __launch_bounds__(256) add_slices_kernel(const float* __restrict__ partial, int32_t n_slices,
+                                                         int32_t h, float* __restrict__ out) {
+  const int col = blockIdx.x * 256 + threadIdx.x;
   if (col >= h) return;
   float s = 0.f;
-  for (int i = 0; i < n_partial; ++i) s += partial[static_cast<int64_t>(i) * h + col];
+  for (int i = 0; i < n_slices; ++i) s += partial[static_cast<int64_t>(i) * 64 * h + col];
   out[col] += s;
 }
 
@@ -265,22 +300,29 @@ hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* gain, uint16_t* y, int
 }
 
 int32_t rmsnorm_bwd_partials(int64_t rows) {
-  int64_t blocks = (rows + 3) / 4;
-  return static_cast<int32_t>(blocks < 256 ? blocks : 256);
+  return static_cast<int32_t>(rows < 1024 ? rows : 1024);     // one block per row, up to four per CU
 }
 
 hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const uint16_t* dy, const uint16_t* dres,
                        uint16_t* dx, float* partial, int32_t n_partial, int64_t rows, int32_t h, float eps,
                        hipStream_t stream) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(rmsnorm_bwd_kernel, dim3(n_partial), dim3(256), 0, stream, x, gain, dy, dres, dx,
-                     partial, rows, h, eps);
+  const int cpl = (h + 2047) / 2048;
+#define L4D_RMS_BWD(C)                                                                                       \
+  hipLaunchKernelGGL(rmsnorm_bwd_kernel<C>, dim3(n_partial), dim3(256), 0, stream, x, gain, dy, dres, dx, \
+                     partial, rows, h, eps)
+  if (cpl <= 1) L4D_RMS_BWD(1);
+  else if (cpl <= 2) L4D_RMS_BWD(2);
+  else L4D_RMS_BWD(4);
+#undef L4D_RMS_BWD
   return hipGetLastError();
 }
 
-hipError_t reduce_rows_add(const float* partial, int32_t n_partial, int32_t h, float* out, hipStream_t stream) {
-  hipLaunchKernelGGL(reduce_rows_add_kernel, dim3((h + 255) / 256), dim3(256), 0, stream, partial, n_partial,
-                     h, out);
+hipError_t reduce_rows_add(float* partial, int32_t n_partial, int32_t h, float* out, hipStream_t stream) {
+  if (n_partial <= 0) return hipSuccess;
+  const int slices = (n_partial + 63) / 64;
+  hipLaunchKernelGGL(reduce_slices_kernel, dim3((h + 63) / 64, slices), dim3(256), 0, stream, partial, n_partial, h);
+  hipLaunchKernelGGL(add_slices_kernel, dim3((h + 255) / 256), dim3(256), 0, stream, partial, slices, h, out);
   return hipGetLastError();
 }
 
