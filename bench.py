@@ -14,8 +14,16 @@ durations come from HIP events that the library records around each launch
 on the launch stream, over the timed steps.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline] [--no-others]
+    python bench.py --calibrate-copy BYTES     # a plain device copy, for HBM counter calibration
+
+roofline.traffic is the dominant kernel's HBM bytes per launch as measured
+by rocprofv3 FETCH_SIZE + WRITE_SIZE (scaled by the counters' reading for a
+plain copy of known size), read from profiles/hbm_traffic_llama2_7b_layer.txt;
+it is null when that file has no entry for the kernel or when the kernel's
+source file has changed since the counters were taken (SHA-256 mismatch).
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -77,6 +85,47 @@ def kernel_work(w):
 
 def lm_flops(w):
     return 3 * 2 * w.tokens * w.v_t * w.hidden
+
+
+# Source file of each kernel family (for the traffic table's staleness check).
+KERNEL_SOURCE = {"gemm": "gemm.hip", "attn": "attention.hip", "rmsnorm": "rowwise.hip", "reduce": "rowwise.hip",
+                 "rope": "rowwise.hip", "xent": "rowwise.hip"}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama2_7b_layer.txt")
+
+
+def source_sha(kernel):
+    src = KERNEL_SOURCE.get(kernel.split("_")[0])
+    if src is None:
+        return None
+    with open(os.path.join(ROOT, "paper_2411_06465_amd", "csrc", src), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch from the committed counter summary, or None when
+    absent or taken on a different version of the kernel's source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    sha = source_sha(kernel)
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            parts = line.split()
+            if len(parts) == 5 and parts[0] == "traffic" and parts[1] == kernel:
+                return int(parts[2]) if parts[4] == sha else None
+    return None
+
+
+def calibrate_copy(nbytes):
+    """A plain device-to-device copy of nbytes, five times (for the HBM counters)."""
+    import torch
+    torch.cuda.set_device(0)
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(f"copied {nbytes} bytes x 5", flush=True)
 
 
 # ------------------------------------------------------------------ runs
@@ -197,7 +246,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-others", action="store_true")
     ap.add_argument("--cpu-seq", type=int, default=1024)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU's shard: the library has no multi-GPU path; run with --gpus 1",
               file=sys.stderr)
@@ -228,7 +281,7 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": round(amount / avg_s / 1e9, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(dom)
     roof["kernel"] = dom
     roof["avg_ms"] = round(total_ms / launches, 4)
 
