@@ -534,8 +534,36 @@ __device__ __forceinline__ void copy2_kc(uint8_t* lds, const Kc2Rows<WAVES>& row
     __builtin_amdgcn_global_load_lds(GPTR(rows.row[q] + k), LPTR(lds + (wave + WAVES * q) * 1024), 16, 0, 0);
 }
 
+// MN copies.  For an operand whose rows are one plain array (no sequence-
+// parallel split) a lane's offset is fixed over K and across its copies up to
+// a uniform stride: copy q reads k-row kr0 + 2 * WAVES * q, and the column
+// swizzle depends on kr mod 4, which q does not change.  One offset per lane
+// is kept; each stage adds one uniform row offset.  A split operand resolves
+// every k-row through RowSrc.
+struct Mn2Rows {
+  uint32_t off0;   // element offset of the lane's 16 bytes for copy 0 at k0 = 0
+};
+
 template <int WAVES>
-__device__ __forceinline__ void copy2_mn(uint8_t* lds, const Operand& op, int x0, int k0, int wave, int lane) {
+__device__ __forceinline__ Mn2Rows mn2_rows(const Operand& op, int x0, int wave, int lane) {
+  const int kr = 2 * wave + (lane >> 5);
+  const int lc = (lane & 31) ^ mn_swz(kr);
+  int x = x0 + lc * 8;
+  if (x >= op.rows) x = op.rows - 8;
+  return Mn2Rows{static_cast<uint32_t>(kr * op.src.ld + x)};
+}
+
+template <int WAVES>
+__device__ __forceinline__ void copy2_mn(uint8_t* lds, const Operand& op, const Mn2Rows& rows, int x0, int k0,
+                                         int wave, int lane) {
+  if (op.src.t == 1) {       // uniform
+#pragma unroll
+    for (int q = 0; q < 32 / WAVES; ++q) {
+      const uint16_t* base = op.src.own + static_cast<int64_t>(k0 + 2 * WAVES * q) * op.src.ld;
+      __builtin_amdgcn_global_load_lds(GPTR(base + rows.off0), LPTR(lds + (wave + WAVES * q) * 1024), 16, 0, 0);
+    }
+    return;
+  }
 #pragma unroll
   for (int q = 0; q < 32 / WAVES; ++q) {
     const int kb = wave + WAVES * q;
@@ -584,6 +612,8 @@ __device__ __forceinline__ void mfma_frags2(f32x16 (&acc)[4][NS], const Frags2<N
 }
 
 // Spread DS reads over the MFMAs of a sub-step: 8 slots of (DS share, M MFMAs).
+// Only when both operands are K-contiguous: with a transposed operand (two
+// transposing reads per fragment) the compiler's own order measured faster.
 template <int DS, int M, int I = 0>
 __device__ __forceinline__ void interleave2_slots() {
   if constexpr (I < 8) {
@@ -595,7 +625,7 @@ __device__ __forceinline__ void interleave2_slots() {
 }
 template <Layout LA, Layout LB, int NS>
 __device__ __forceinline__ void interleave2() {
-  interleave2_slots<4 * (LA == Layout::KC ? 1 : 2) + NS * (LB == Layout::KC ? 1 : 2), NS / 2>();
+  if constexpr (LA == Layout::KC && LB == Layout::KC) interleave2_slots<4 + NS, NS / 2>();
 }
 
 template <Layout LA, Layout LB, EpiKind KIND, int PAIR, int WAVES>
@@ -622,13 +652,16 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
     for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
 
   Kc2Rows<WAVES> ra{}, rb{};
+  Mn2Rows ma{}, mb{};
   if constexpr (LA == Layout::KC) ra = kc2_rows<WAVES>(p.A, m0, tm, wave, lane);
+  else ma = mn2_rows<WAVES>(p.A, m0, wave, lane);
   if constexpr (LB == Layout::KC) rb = kc2_rows<WAVES>(p.B, n0, tn, wave, lane);
+  else mb = mn2_rows<WAVES>(p.B, n0, wave, lane);
   auto issue = [&](int k0, uint8_t* la, uint8_t* lb) {
     if constexpr (LA == Layout::KC) copy2_kc<WAVES>(la, ra, k0, wave);
-    else copy2_mn<WAVES>(la, p.A, m0, k0, wave, lane);
+    else copy2_mn<WAVES>(la, p.A, ma, m0, k0, wave, lane);
     if constexpr (LB == Layout::KC) copy2_kc<WAVES>(lb, rb, k0, wave);
-    else copy2_mn<WAVES>(lb, p.B, n0, k0, wave, lane);
+    else copy2_mn<WAVES>(lb, p.B, mb, n0, k0, wave, lane);
   };
 
   // K is a multiple of 2 * BK2 (the host picks this kernel only then).
