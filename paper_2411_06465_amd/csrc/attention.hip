@@ -214,7 +214,8 @@ template <int D>
 __global__ void __launch_bounds__(256, 1) attn_fwd_kernel(AttnParams p) {
   constexpr int TB = KT * D * 2;
   __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB], k2[TB], v2[TB];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave: scalar code for wave-level decisions
   const int n_qt = (p.n_q + 127) / 128;
   const int qt = n_qt - 1 - blockIdx.x;         // heaviest tiles first
   const int hq = blockIdx.y, bi = blockIdx.z;
@@ -375,7 +376,8 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkdv_kernel(AttnParams p) {
   constexpr int TB = QT * D * 2;
   __shared__ __attribute__((aligned(16))) uint8_t q0[TB], g0[TB], q1[TB], g1[TB], q2[TB], g2[TB];   // Q, dO tiles
   __shared__ __attribute__((aligned(16))) float st0[2][QT], st1[2][QT], st2[2][QT];                  // lse, delta
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = tid >> 6;   // per-lane here: the scalar form raised register pressure into spills
   const int group = p.a_t / p.k_t;
   const int hpb = group / p.n_split;
   const int hk = blockIdx.y / p.n_split, split = blockIdx.y % p.n_split;
@@ -615,7 +617,8 @@ template <int D>
 __global__ void __launch_bounds__(256, 1) attn_bwd_dq_kernel(AttnParams p) {
   constexpr int TB = KT * D * 2;
   __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB], k2[TB], v2[TB];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave: scalar code for wave-level decisions
   const int n_qt = (p.n_q + 127) / 128;
   const int qt = n_qt - 1 - blockIdx.x;
   const int hq = blockIdx.y, bi = blockIdx.z;

@@ -402,7 +402,8 @@ __global__ void __launch_bounds__(512, 1) gemm_bk32(GemmParams p) {
   constexpr bool RAGGED = true;
   __shared__ __attribute__((aligned(16))) uint8_t a0[TILE_BYTES], b0[TILE_BYTES], a1[TILE_BYTES], b1[TILE_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t a2[TILE_BYTES], b2[TILE_BYTES], a3[TILE_BYTES], b3[TILE_BYTES];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave: scalar code for wave-level decisions
   const TileCoord tc = tile_of(p);
   const int tm = tc.tm, tn = tc.tn, m0 = tm * BM, n0 = tn * BN;
   const int wm = wave >> 2, wn = wave & 3;
@@ -633,7 +634,8 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   constexpr int NS = WAVES == 8 ? 2 : 4;
   constexpr int PER = 32 / WAVES;           // copy instructions per operand per stage per wave
   __shared__ __attribute__((aligned(16))) uint8_t a0[TILE2], b0[TILE2], a1[TILE2], b1[TILE2];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave: scalar code for wave-level decisions
   const TileCoord tc = tile_of(p);
   const int tm = tc.tm, tn = tc.tn, m0 = tm * BM, n0 = tn * BN;
   const int wm = WAVES == 8 ? (wave >> 2) : (wave >> 1);
