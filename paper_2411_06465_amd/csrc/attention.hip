@@ -83,20 +83,32 @@ __device__ __forceinline__ int t_off(int row, int chunk) {
 
 // Copy rows [0, ROWS) of src (row stride ld, rows >= n_valid clamped to the
 // last valid row) into an LDS tile; the four waves of the block share the work.
+// A copy instruction moves RPK whole rows (1 KB); lane i lands at byte 16 i of
+// the instruction's LDS chunk.  The wave's copies all start at rows of the same
+// parity, so each lane's swizzled source column is fixed: the address is a
+// uniform row base plus one per-lane 32-bit offset, except on a ragged tail.
 template <int D, int ROWS>
 __device__ __forceinline__ void tile_load(uint8_t* lds, const uint16_t* src, int64_t ld, int n_valid, int wave,
                                           int lane) {
   constexpr int CH = D / 8;              // 16-byte chunks per row
   constexpr int RPK = 64 / CH;           // rows per 1 KB wave chunk
   constexpr int NKB = ROWS / RPK;
-  const int last = n_valid - 1;
+  static_assert(NKB % 4 == 0 || NKB < 4, "copies are dealt to 4 waves");
+  const int lrow = lane / CH;
+  const int lc = (lane % CH) ^ swz<D>(wave * RPK + lrow);   // row parity of every copy of this wave
+  const uint32_t lane_off = static_cast<uint32_t>(lrow * ld + lc * 8);
+  if (n_valid >= ROWS) {
 #pragma unroll
-  for (int q = wave; q < NKB; q += 4) {
-    const int row = q * RPK + lane / CH;
-    const int lc = (lane % CH) ^ swz<D>(row);
-    const int r = row < last ? row : last;
-    __builtin_amdgcn_global_load_lds(GPTR(src + static_cast<int64_t>(r) * ld + lc * 8), LPTR(lds + q * 1024), 16, 0,
-                                     0);
+    for (int q = wave; q < NKB; q += 4)
+      __builtin_amdgcn_global_load_lds(GPTR(src + static_cast<int64_t>(q * RPK) * ld + lane_off),
+                                       LPTR(lds + q * 1024), 16, 0, 0);
+  } else {                               // ragged tail: rows past n_valid repeat the last valid row
+#pragma unroll
+    for (int q = wave; q < NKB; q += 4) {
+      const int r = min(q * RPK + lrow, n_valid - 1);
+      __builtin_amdgcn_global_load_lds(GPTR(src + static_cast<int64_t>(r) * ld + lc * 8), LPTR(lds + q * 1024), 16,
+                                       0, 0);
+    }
   }
 }
 
@@ -209,16 +221,41 @@ __device__ __forceinline__ void run_ring(int total, Next next, Issue issue, Comp
 }
 
 // ------------------------------------------------------------------ forward
-// grid: (q tiles of 128, a_t heads, b); 4 waves x 32 queries.
+// One workgroup per (128-query tile, query head, batch element); 4 waves x 32
+// queries, each lane holding one query's scores (S^T = K Q^T).  The launch is
+// one-dimensional with the head index varying fastest and the query tiles in
+// descending order, so the longest causal rows are dispatched first across all
+// heads.  Registers stay within 256 per lane and LDS within 64 KB, so two
+// workgroups share a CU and each SIMD interleaves the matrix products of one
+// wave with the softmax of another.
+//
+// The output and the row sum are rescaled only on tiles where some row's
+// maximum grew (a wave-wide vote).  The reference maximum stays exact: a
+// stale one would leave the largest probability of a row off the bf16 grid
+// point 1 and, for sharply peaked rows, double the rounding error of ctx.
+
+// Next key tile to visit at or after (seg, t0): the first tile of a segment
+// whose first key a query at pos_max can see.  Positions grow within a
+// segment, so the rest of a segment is skipped once a tile starts past pos_max.
+__device__ __forceinline__ bool next_tile(const AttnParams& p, int pos_max, int& seg, int& t0) {
+  while (seg < p.n_seg) {
+    if (t0 < p.seg[seg].n && p.seg[seg].pos0 + t0 <= pos_max) return true;
+    ++seg;
+    t0 = 0;
+  }
+  return false;
+}
+
 template <int D>
-__global__ void __launch_bounds__(256, 1) attn_fwd_kernel(AttnParams p) {
+__global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
   constexpr int TB = KT * D * 2;
-  __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB], k2[TB], v2[TB];
+  __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB];
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave: scalar code for wave-level decisions
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n_qt = (p.n_q + 127) / 128;
-  const int qt = n_qt - 1 - blockIdx.x;         // heaviest tiles first
-  const int hq = blockIdx.y, bi = blockIdx.z;
+  const int nh = p.a_t * p.b;
+  const int qt = n_qt - 1 - static_cast<int>(blockIdx.x) / nh;   // heaviest tiles first
+  const int hq = static_cast<int>(blockIdx.x) % nh % p.a_t, bi = static_cast<int>(blockIdx.x) % nh / p.a_t;
   const int hk = hq / (p.a_t / p.k_t);
   const int q_row0 = qt * 128;
   const int my_q = q_row0 + wave * 32 + (lane & 31);
@@ -240,7 +277,6 @@ __global__ void __launch_bounds__(256, 1) attn_fwd_kernel(AttnParams p) {
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) o[i] = f32x16{};
 
-  const int ntiles = total_tiles(p, KT);
   auto issue = [&](int seg, int t0, uint8_t* kt, uint8_t* vt) __attribute__((always_inline)) {
     const KvSeg& s = p.seg[seg];
     const int64_t off = bi * s.bstride + static_cast<int64_t>(t0) * s.ld + hk * D;
@@ -248,9 +284,8 @@ __global__ void __launch_bounds__(256, 1) attn_fwd_kernel(AttnParams p) {
     tile_load<D, KT>(vt, s.v + off, s.ld, s.n - t0, wave, lane);
   };
   auto compute = [&](int seg, int t0, const uint8_t* kt, const uint8_t* vt) __attribute__((always_inline)) {
-    const KvSeg& s = p.seg[seg];
-    const int kpos0 = s.pos0 + t0;
-    const int kvalid = min(KT, s.n - t0);
+    const int kpos0 = p.seg[seg].pos0 + t0;
+    const int kvalid = min(KT, p.seg[seg].n - t0);
     f32x16 sc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk)
@@ -264,15 +299,21 @@ __global__ void __launch_bounds__(256, 1) attn_fwd_kernel(AttnParams p) {
         for (int i = 0; i < 16; ++i)
           if (t2 * 32 + 8 * (i >> 2) + rbase + (i & 3) > lim) sc[t2][i] = -INFINITY;
     }
-    float mx = -INFINITY;
+    float mx = fmaxf(sc[0][0], sc[0][1]);
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2)
+    for (int i = 2; i < 16; i += 2) mx = fmaxf(mx, fmaxf(sc[0][i], sc[0][i + 1]));
 #pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[t2][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx * c);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
+    for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(sc[1][i], sc[1][i + 1]));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
+    if (__builtin_amdgcn_ballot_w64(mx > m_run)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);   // 0 while m_run is -inf
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
+      l_run *= alpha;
+      m_run = m_new;
+    }
+    const float m_use = m_run == -INFINITY ? 0.f : m_run;
     float rs = 0.f;
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2)
@@ -282,12 +323,7 @@ __global__ void __launch_bounds__(256, 1) attn_fwd_kernel(AttnParams p) {
         sc[t2][i] = pr;
         rs += pr;
       }
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-    if (__ballot(alpha != 1.0f)) {
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
-    }
+    l_run += rs;
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
@@ -298,32 +334,32 @@ __global__ void __launch_bounds__(256, 1) attn_fwd_kernel(AttnParams p) {
       }
   };
 
-  auto kbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
-    if constexpr (decltype(b)::value == 0) return k0;
-    else if constexpr (decltype(b)::value == 1) return k1;
-    else return k2;
-  };
-  auto vbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
-    if constexpr (decltype(b)::value == 0) return v0;
-    else if constexpr (decltype(b)::value == 1) return v1;
-    else return v2;
-  };
-  run_ring<KT * D / 1024>(
-      ntiles,
-      [&](int from) __attribute__((always_inline)) {
-        int s_, t_;
-        return next_key_tile(p, from, ntiles, pos_max, s_, t_);
-      },
-      [&](int t, auto b) __attribute__((always_inline)) {
-        int s_, t_;
-        find_tile(p, t, KT, s_, t_);
-        issue(s_, t_, kbuf(b), vbuf(b));
-      },
-      [&](int t, auto b) __attribute__((always_inline)) {
-        int s_, t_;
-        find_tile(p, t, KT, s_, t_);
-        compute(s_, t_, kbuf(b), vbuf(b));
-      });
+  // Two-stage ring: tile j computes from one buffer pair while tile j+1 lands
+  // in the other.
+  int cs = 0, ct = 0;
+  bool have = next_tile(p, pos_max, cs, ct);
+  if (have) issue(cs, ct, k0, v0);
+  while (have) {
+    int ns = cs, nt = ct + KT;
+    bool more = next_tile(p, pos_max, ns, nt);
+    wait_copies<0>();
+    ring_barrier();
+    if (more) issue(ns, nt, k1, v1);
+    compute(cs, ct, k0, v0);
+    if (!more) break;
+    cs = ns;
+    ct = nt;
+    ns = cs;
+    nt = ct + KT;
+    more = next_tile(p, pos_max, ns, nt);
+    wait_copies<0>();
+    ring_barrier();
+    if (more) issue(ns, nt, k0, v0);
+    compute(cs, ct, k1, v1);
+    have = more;
+    cs = ns;
+    ct = nt;
+  }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (!q_ok) return;
@@ -337,8 +373,10 @@ __global__ void __launch_bounds__(256, 1) attn_fwd_kernel(AttnParams p) {
       *reinterpret_cast<u32x2*>(ob + d) = u32x2{pack2(o[dt][4 * jj] * inv, o[dt][4 * jj + 1] * inv),
                                                 pack2(o[dt][4 * jj + 2] * inv, o[dt][4 * jj + 3] * inv)};
     }
-  if (lane < 32)
-    p.lse[(static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + my_q] = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
+  if (lane < 32) {
+    const float m_fin = m_run == -INFINITY ? 0.f : m_run;
+    p.lse[(static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + my_q] = (m_fin + __builtin_amdgcn_logf(l_tot)) * kLn2;
+  }
 }
 
 // ------------------------------------------------------------------ backward: delta
@@ -746,7 +784,8 @@ int count_blocks(const AttnParams& p, int tsz) {
 
 template <int D>
 hipError_t fwd_impl(const AttnParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3((p.n_q + 127) / 128, p.a_t, p.b), dim3(256), 0, stream, p);
+  const unsigned blocks = static_cast<unsigned>((p.n_q + 127) / 128) * p.a_t * p.b;
+  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3(blocks), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 
