@@ -82,32 +82,39 @@ __device__ __forceinline__ int t_off(int row, int chunk) {
 }
 
 // Copy rows [0, ROWS) of src (row stride ld, rows >= n_valid clamped to the
-// last valid row) into an LDS tile; the four waves of the block share the work.
+// last valid row) into an LDS tile; the NW waves of the block share the work.
 // A copy instruction moves RPK whole rows (1 KB); lane i lands at byte 16 i of
 // the instruction's LDS chunk.  The wave's copies all start at rows of the same
-// parity, so each lane's swizzled source column is fixed: the address is a
-// uniform row base plus one per-lane 32-bit offset, except on a ragged tail.
-template <int D, int ROWS>
+// parity, so each lane's swizzled source column is fixed: a buffer load with
+// the tile base in the (uniform) resource, the row block in the scalar offset
+// and one 32-bit per-lane offset, except on a ragged tail.
+constexpr int kBufferDword3 = 0x00020000;    // raw buffer, 32-bit data format (gfx9 family)
+template <int D, int ROWS, int NW = 4>
 __device__ __forceinline__ void tile_load(uint8_t* lds, const uint16_t* src, int64_t ld, int n_valid, int wave,
                                           int lane) {
   constexpr int CH = D / 8;              // 16-byte chunks per row
   constexpr int RPK = 64 / CH;           // rows per 1 KB wave chunk
   constexpr int NKB = ROWS / RPK;
-  static_assert(NKB % 4 == 0 || NKB < 4, "copies are dealt to 4 waves");
+  static_assert(NKB % NW == 0, "every wave issues the same number of copies");
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(src), 0, -1, kBufferDword3);
   const int lrow = lane / CH;
   const int lc = (lane % CH) ^ swz<D>(wave * RPK + lrow);   // row parity of every copy of this wave
-  const uint32_t lane_off = static_cast<uint32_t>(lrow * ld + lc * 8);
+  const int ldb = static_cast<int>(ld) * 2;                 // row stride in bytes
   if (n_valid >= ROWS) {
+    const uint32_t lane_off = static_cast<uint32_t>(lrow * ldb + lc * 16);
 #pragma unroll
-    for (int q = wave; q < NKB; q += 4)
-      __builtin_amdgcn_global_load_lds(GPTR(src + static_cast<int64_t>(q * RPK) * ld + lane_off),
-                                       LPTR(lds + q * 1024), 16, 0, 0);
+    for (int j = 0; j < NKB / NW; ++j) {
+      const int q = wave + j * NW;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LPTR(lds + q * 1024), 16, lane_off, q * RPK * ldb, 0, 0);
+    }
   } else {                               // ragged tail: rows past n_valid repeat the last valid row
 #pragma unroll
-    for (int q = wave; q < NKB; q += 4) {
+    for (int j = 0; j < NKB / NW; ++j) {
+      const int q = wave + j * NW;
       const int r = min(q * RPK + lrow, n_valid - 1);
-      __builtin_amdgcn_global_load_lds(GPTR(src + static_cast<int64_t>(r) * ld + lc * 8), LPTR(lds + q * 1024), 16,
-                                       0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LPTR(lds + q * 1024), 16, static_cast<uint32_t>(r * ldb + lc * 16),
+                                               0, 0, 0);
     }
   }
 }
@@ -246,6 +253,42 @@ __device__ __forceinline__ bool next_tile(const AttnParams& p, int pos_max, int&
   return false;
 }
 
+// Two-stage copy ring over the key tiles of `step` keys that a query at
+// pos_max can see: tile j is computed from buffer j % 2 while tile j + 1 lands
+// in the other.  `issue(seg, t0, buf)` starts a tile's copies, `compute(seg,
+// t0, buf)` uses it; buf is std::integral_constant<int, 0 or 1>, so every LDS
+// object is named statically and the compiler sees that reads of one buffer
+// do not depend on the copies landing in the other.
+template <class Issue, class Compute>
+__device__ __forceinline__ void run_ring2(const AttnParams& p, int pos_max, int step, Issue issue, Compute compute) {
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  int cs = 0, ct = 0;
+  bool have = next_tile(p, pos_max, cs, ct);
+  if (have) issue(cs, ct, B0{});
+  while (have) {
+    int ns = cs, nt = ct + step;
+    bool more = next_tile(p, pos_max, ns, nt);
+    wait_copies<0>();
+    ring_barrier();                      // every wave's copy is visible; the other buffer is free
+    if (more) issue(ns, nt, B1{});
+    compute(cs, ct, B0{});
+    if (!more) break;
+    cs = ns;
+    ct = nt;
+    ns = cs;
+    nt = ct + step;
+    more = next_tile(p, pos_max, ns, nt);
+    wait_copies<0>();
+    ring_barrier();
+    if (more) issue(ns, nt, B0{});
+    compute(cs, ct, B1{});
+    have = more;
+    cs = ns;
+    ct = nt;
+  }
+}
+
 template <int D>
 __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
   constexpr int TB = KT * D * 2;
@@ -292,12 +335,13 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
 #pragma unroll
       for (int t2 = 0; t2 < 2; ++t2) sc[t2] = mfma(frag_rows<D>(kt, t2 * 32, kk, lane), qf[kk], sc[t2]);
     if (kpos0 + KT - 1 > pos_min || kvalid < KT) {       // tile straddles the diagonal (or is ragged)
-      const int lim = min(my_pos - kpos0, kvalid - 1);   // last visible key row for this query
+      // last visible key row for this query, relative to the lane's first row
+      const int lim = min(my_pos - kpos0, kvalid - 1) - rbase;
 #pragma unroll
       for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-          if (t2 * 32 + 8 * (i >> 2) + rbase + (i & 3) > lim) sc[t2][i] = -INFINITY;
+          if (t2 * 32 + 8 * (i >> 2) + (i & 3) > lim) sc[t2][i] = -INFINITY;
     }
     float mx = fmaxf(sc[0][0], sc[0][1]);
 #pragma unroll
@@ -334,32 +378,16 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
       }
   };
 
-  // Two-stage ring: tile j computes from one buffer pair while tile j+1 lands
-  // in the other.
-  int cs = 0, ct = 0;
-  bool have = next_tile(p, pos_max, cs, ct);
-  if (have) issue(cs, ct, k0, v0);
-  while (have) {
-    int ns = cs, nt = ct + KT;
-    bool more = next_tile(p, pos_max, ns, nt);
-    wait_copies<0>();
-    ring_barrier();
-    if (more) issue(ns, nt, k1, v1);
-    compute(cs, ct, k0, v0);
-    if (!more) break;
-    cs = ns;
-    ct = nt;
-    ns = cs;
-    nt = ct + KT;
-    more = next_tile(p, pos_max, ns, nt);
-    wait_copies<0>();
-    ring_barrier();
-    if (more) issue(ns, nt, k0, v0);
-    compute(cs, ct, k1, v1);
-    have = more;
-    cs = ns;
-    ct = nt;
-  }
+  run_ring2(
+      p, pos_max, KT,
+      [&](int seg, int t0, auto b) __attribute__((always_inline)) {
+        if constexpr (decltype(b)::value == 0) issue(seg, t0, k0, v0);
+        else issue(seg, t0, k1, v1);
+      },
+      [&](int seg, int t0, auto b) __attribute__((always_inline)) {
+        if constexpr (decltype(b)::value == 0) compute(seg, t0, k0, v0);
+        else compute(seg, t0, k1, v1);
+      });
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (!q_ok) return;
@@ -406,16 +434,68 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(AttnParams p) {
   }
 }
 
-// ------------------------------------------------------------------ backward: dK, dV
-// grid: (key blocks of 128 over all segments, k_t * n_split, b); 4 waves x 32 keys.
-// Workgroup (kb, hk, split) sums over query heads hk*g + [split*hpb, (split+1)*hpb).
+// s[h] += A[32 h + (0..31)] x^T over the tile's D columns, with A the LDS
+// tile and x the lane's 32 key rows (K or V) in registers: S^T or dP^T for 64
+// queries.  The schedule keeps two fragment reads ahead of the products, so
+// at most three fragments are live instead of all sixteen.
 template <int D>
-__global__ void __launch_bounds__(256, 1) attn_bwd_dkdv_kernel(AttnParams p) {
+__device__ __forceinline__ void scores_t(const uint8_t* lds, const bf16x8 (&x)[D / 16], f32x16 (&s)[2], int lane) {
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) s[h] = mfma(frag_rows<D>(lds, 32 * h, kk, lane), x[kk], s[h]);
+  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);      // LDS reads
+#pragma unroll
+  for (int i = 0; i < D / 8 - 2; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+}
+
+// acc[dt] += A^T x over 64 queries: A the LDS tile read transposed (d rows,
+// query contraction) and x[g] the bf16 P^T or dS^T of query group g from
+// registers: dV^T or dK^T.  Two fragment reads stay ahead of the products.
+template <int D>
+__device__ __forceinline__ void accum_t(const uint8_t* lds, const bf16x8 (&x)[4], f32x16 (&acc)[D / 32], int lane) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) acc[dt] = mfma(frag_cols<D>(lds, dt, g, lane), x[g], acc[dt]);
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);      // LDS reads (two per fragment)
+#pragma unroll
+  for (int i = 0; i < D / 8 - 2; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+}
+
+// ------------------------------------------------------------------ backward: dK, dV
+// grid: (key blocks of 128 over all segments, k_t * n_split, b); 8 waves.
+// Workgroup (kb, hk, split) sums over query heads hk*g + [split*hpb, (split+1)*hpb).
+//
+// The block's 128 keys form four groups of 32, and each group has two waves
+// with different jobs, on the same SIMD (wave w runs on SIMD w % 4):
+//  * role 0 (waves 0-3) holds K, computes S^T = K Q^T, P^T = exp(S^T - lse),
+//    hands P^T (bf16) to its partner through LDS and accumulates dV^T += dO^T P^T;
+//  * role 1 (waves 4-7) holds V, computes dP^T = V dO^T, takes P^T and forms
+//    dS^T = P^T (dP^T - delta), and accumulates dK^T += Q^T dS^T.
+// Each wave then needs one operand block and one accumulator block, which fits
+// 256 registers, and the two waves of a SIMD issue different instruction mixes
+// (softmax on one, products on the other) that interleave.  Both use the same
+// bf16 P^T, the one dV is built from.
+template <int D>
+__global__ void __launch_bounds__(512, 2) attn_bwd_dkdv_kernel(AttnParams p) {
   constexpr int TB = QT * D * 2;
-  __shared__ __attribute__((aligned(16))) uint8_t q0[TB], g0[TB], q1[TB], g1[TB], q2[TB], g2[TB];   // Q, dO tiles
-  __shared__ __attribute__((aligned(16))) float st0[2][QT], st1[2][QT], st2[2][QT];                  // lse, delta
+  // Two stages of Q and dO tiles (64 KB at D = 128: every tile offset fits a
+  // ds_read immediate), then the statistics and the P^T handover.
+  __shared__ __attribute__((aligned(16))) uint8_t q0[TB], g0[TB], q1[TB], g1[TB];   // Q, dO tiles
+  __shared__ __attribute__((aligned(16))) float st0[2][QT], st1[2][QT];             // lse, delta
+  __shared__ __attribute__((aligned(16))) u32x4 xp[4][QT / 16][64];    // P^T handover: [group][16 queries][lane]
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = tid >> 6;   // per-lane here: the scalar form raised register pressure into spills
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave & 3, role = wave >> 2;
   const int group = p.a_t / p.k_t;
   const int hpb = group / p.n_split;
   const int hk = blockIdx.y / p.n_split, split = blockIdx.y % p.n_split;
@@ -423,29 +503,24 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkdv_kernel(AttnParams p) {
   int seg, k0;
   if (!find_tile(p, blockIdx.x, 128, seg, k0)) return;
   const KvSeg& S = p.seg[seg];
-  const int my_key = k0 + wave * 32 + (lane & 31);
+  const int my_key = k0 + grp * 32 + (lane & 31);
   const bool key_ok = my_key < S.n;
   const int my_kpos = S.pos0 + my_key;
-  const int wave_kpos0 = S.pos0 + k0 + wave * 32;
+  const int grp_kpos0 = S.pos0 + k0 + grp * 32;
   const int blk_kpos0 = S.pos0 + k0;
   const int rbase = 4 * (lane >> 5);
 
-  bf16x8 kf[D / 16], vf[D / 16];
+  bf16x8 kv[D / 16];                     // role 0: K rows, role 1: V rows of the group's keys
   {
+    const uint16_t* src = role == 0 ? S.k : S.v;
     const int64_t off = bi * S.bstride + static_cast<int64_t>(key_ok ? my_key : 0) * S.ld + hk * D;
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-      const int dcol = (2 * kk + (lane >> 5)) * 8;
-      kf[kk] = *reinterpret_cast<const bf16x8*>(S.k + off + dcol);
-      vf[kk] = *reinterpret_cast<const bf16x8*>(S.v + off + dcol);
-    }
+    for (int kk = 0; kk < D / 16; ++kk)
+      kv[kk] = *reinterpret_cast<const bf16x8*>(src + off + (2 * kk + (lane >> 5)) * 8);
   }
-  f32x16 dk[D / 32], dv[D / 32];
+  f32x16 acc[D / 32];                    // role 0: dV^T, role 1: dK^T (d rows, the lane's key)
 #pragma unroll
-  for (int i = 0; i < D / 32; ++i) {
-    dk[i] = f32x16{};
-    dv[i] = f32x16{};
-  }
+  for (int i = 0; i < D / 32; ++i) acc[i] = f32x16{};
   const float c = p.scale * kLog2e;
   const int n_qt = (p.n_q + QT - 1) / QT;
   const int total = hpb * n_qt;
@@ -460,129 +535,156 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkdv_kernel(AttnParams p) {
   };
   auto issue = [&](int it, uint8_t* qt_l, uint8_t* gt_l, float (*st)[QT]) __attribute__((always_inline)) {
     const int hq = head0 + it / n_qt, qt = it % n_qt;
-    if (lane < 16) {    // wave w copies the statistics of queries 16w .. 16w+15 (rows past n_q: the last row)
-      const int q = min(qt * QT + wave * 16 + lane, p.n_q - 1);
+    if (lane < 16) {    // waves 0-3 copy the lse, waves 4-7 delta, of queries 16 grp .. 16 grp + 15
+      const int q = min(qt * QT + grp * 16 + lane, p.n_q - 1);
       const int64_t idx = (static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + q;
-      __builtin_amdgcn_global_load_lds(GPTR(p.lse + idx), LPTR(&st[0][wave * 16]), 4, 0, 0);
-      __builtin_amdgcn_global_load_lds(GPTR(p.delta + idx), LPTR(&st[1][wave * 16]), 4, 0, 0);
+      __builtin_amdgcn_global_load_lds(GPTR((role == 0 ? p.lse : p.delta) + idx), LPTR(&st[role][grp * 16]), 4, 0,
+                                       0);
     }
     const int64_t off = bi * p.q_bstride + static_cast<int64_t>(qt * QT) * p.q_ld + hq * D;
-    tile_load<D, QT>(qt_l, p.q + off, p.q_ld, p.n_q - qt * QT, wave, lane);
-    tile_load<D, QT>(gt_l, p.dout + off, p.q_ld, p.n_q - qt * QT, wave, lane);
+    tile_load<D, QT, 8>(qt_l, p.q + off, p.q_ld, p.n_q - qt * QT, wave, lane);
+    tile_load<D, QT, 8>(gt_l, p.dout + off, p.q_ld, p.n_q - qt * QT, wave, lane);
   };
-  // One query tile: the wave's 32 keys against 64 queries as two 32-query
-  // halves, so S^T and dP^T run as four independent MFMA chains.
+  // One query tile (64 queries as four 16-query groups g; MFMA halves h = g / 2).
   auto compute = [&](int it, const uint8_t* qt_l, const uint8_t* gt_l, const float (*st)[QT]) __attribute__((always_inline)) {
     const int qt = it % n_qt;
     const int qr0 = qt * QT;
     const int qlast = min(qr0 + QT - 1, p.n_q - 1);
     const int qp0 = qpos(p.qmap, qr0), qpl = qpos(p.qmap, qlast);
-    if (qpl < wave_kpos0) return;                        // every query of the tile precedes this wave's keys
-    f32x16 sc[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        sc[h] = mfma(frag_rows<D>(qt_l, 32 * h, kk, lane), kf[kk], sc[h]);
-        dp[h] = mfma(frag_rows<D>(gt_l, 32 * h, kk, lane), vf[kk], dp[h]);
-      }
-    const bool full = qp0 >= wave_kpos0 + 31 && qlast == qr0 + QT - 1 && qpl - qp0 == QT - 1;
+    const bool active = qpl >= grp_kpos0;              // some query of the tile sees a key of the group
+    const bool full = qp0 >= grp_kpos0 + 31 && qlast == qr0 + QT - 1 && qpl - qp0 == QT - 1;
     const bool contiguous = qpl - qp0 == qlast - qr0;
+    f32x16 s[2] = {f32x16{}, f32x16{}};              // role 0: S^T -> P^T, role 1: dP^T -> dS^T
+    if (active) {
+      if (role == 0) scores_t<D>(qt_l, kv, s, lane);
+      else scores_t<D>(gt_l, kv, s, lane);
+      if (role == 0) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const float4 ls = *reinterpret_cast<const float4*>(&st[0][32 * h + 8 * jj + rbase]);
-        const float4 de = *reinterpret_cast<const float4*>(&st[1][32 * h + 8 * jj + rbase]);
-        const float lsv[4] = {ls.x * kLog2e, ls.y * kLog2e, ls.z * kLog2e, ls.w * kLog2e};
-        const float dev[4] = {de.x, de.y, de.z, de.w};
+          for (int jj = 0; jj < 4; ++jj) {
+            const float4 ls = *reinterpret_cast<const float4*>(&st[0][32 * h + 8 * jj + rbase]);
+            const float lsv[4] = {ls.x * kLog2e, ls.y * kLog2e, ls.z * kLog2e, ls.w * kLog2e};
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int i = 4 * jj + u;
-          float pr = fast_exp2(fmaf(sc[h][i], c, -lsv[u]));
-          if (!full) {
-            const int qr = 32 * h + 8 * jj + rbase + u;
-            const int qp = contiguous ? qp0 + qr : (qr0 + qr <= qlast ? qpos(p.qmap, qr0 + qr) : -1);
-            if (qr0 + qr > qlast || my_kpos > qp || !key_ok) pr = 0.f;
+            for (int u = 0; u < 4; ++u) s[h][4 * jj + u] = fast_exp2(fmaf(s[h][4 * jj + u], c, -lsv[u]));
           }
-          sc[h][i] = pr;
-          dp[h][i] = pr * (dp[h][i] - dev[u]);
+        if (!full) {                                   // causal / ragged masks
+          if (contiguous) {
+            // visible query rows r (relative to the lane's first row): lo <= r <= hi
+            const int lo = (key_ok ? my_kpos - qp0 : QT) - rbase;
+            const int hi = qlast - qr0 - rbase;
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+              for (int i = 0; i < 16; ++i) {
+                const int r = 32 * h + 8 * (i >> 2) + (i & 3);
+                if (r < lo || r > hi) s[h][i] = 0.f;
+              }
+          } else {                                     // the tile spans two context-parallel chunks
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+              for (int i = 0; i < 16; ++i) {
+                const int qr = 32 * h + 8 * (i >> 2) + rbase + (i & 3);
+                const int qp = qr0 + qr <= qlast ? qpos(p.qmap, qr0 + qr) : -1;
+                if (my_kpos > qp || !key_ok) s[h][i] = 0.f;
+              }
+          }
         }
-      }
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {                        // 16-query groups
-      const bf16x8 pf = frag_acc(sc[g >> 1], 8 * (g & 1));
-      const bf16x8 sf = frag_acc(dp[g >> 1], 8 * (g & 1));
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) {
-        dv[dt] = mfma(frag_cols<D>(gt_l, dt, g, lane), pf, dv[dt]);
-        dk[dt] = mfma(frag_cols<D>(qt_l, dt, g, lane), sf, dk[dt]);
+        for (int g = 0; g < 4; ++g) xp[grp][g][lane] = __builtin_bit_cast(u32x4, frag_acc(s[g >> 1], 8 * (g & 1)));
       }
+    }
+    ring_barrier();                                    // P^T of every group is visible to its partner
+    if (!active) return;
+    if (role == 0) {
+      bf16x8 pf[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) pf[g] = __builtin_bit_cast(bf16x8, xp[grp][g][lane]);
+      __builtin_amdgcn_sched_barrier(0);
+      accum_t<D>(gt_l, pf, acc, lane);
+    } else {
+      // dS^T for all four query groups first, so dP^T is dead before the products start
+      bf16x8 sf[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const u32x4 pp = xp[grp][g][lane];
+        const int h = g >> 1, i0 = 8 * (g & 1);
+        const float4 d0 = *reinterpret_cast<const float4*>(&st[1][32 * h + (i0 >> 2) * 8 + rbase]);
+        const float4 d1 = *reinterpret_cast<const float4*>(&st[1][32 * h + ((i0 >> 2) + 1) * 8 + rbase]);
+        const float dev[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+        float ds[8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          ds[2 * j] = lo16(pp[j]) * (s[h][i0 + 2 * j] - dev[2 * j]);
+          ds[2 * j + 1] = hi16(pp[j]) * (s[h][i0 + 2 * j + 1] - dev[2 * j + 1]);
+        }
+        sf[g] = __builtin_bit_cast(
+            bf16x8, u32x4{pack2(ds[0], ds[1]), pack2(ds[2], ds[3]), pack2(ds[4], ds[5]), pack2(ds[6], ds[7])});
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      accum_t<D>(qt_l, sf, acc, lane);
     }
   };
 
-  auto qbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
-    if constexpr (decltype(b)::value == 0) return q0;
-    else if constexpr (decltype(b)::value == 1) return q1;
-    else return q2;
-  };
-  auto gbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
-    if constexpr (decltype(b)::value == 0) return g0;
-    else if constexpr (decltype(b)::value == 1) return g1;
-    else return g2;
-  };
-  auto sbuf = [&](auto b) __attribute__((always_inline)) -> float (*)[QT] {
-    if constexpr (decltype(b)::value == 0) return st0;
-    else if constexpr (decltype(b)::value == 1) return st1;
-    else return st2;
-  };
-  run_ring<QT * D / 1024 + 2>(     // Q and dO tiles (QT * D * 2 bytes each over 4 waves), lse, delta
-      total, next_wanted, [&](int it, auto b) __attribute__((always_inline)) { issue(it, qbuf(b), gbuf(b), sbuf(b)); },
-      [&](int it, auto b) __attribute__((always_inline)) { compute(it, qbuf(b), gbuf(b), sbuf(b)); });
+  // Two-stage ring over the query tiles: tile j is used from one buffer set
+  // while tile j + 1 lands in the other.
+  int cur = next_wanted(0);
+  if (cur < total) issue(cur, q0, g0, st0);
+  while (cur < total) {
+    int nxt = next_wanted(cur + 1);
+    wait_copies<0>();
+    ring_barrier();                      // tile cur is visible; the other buffers are free
+    if (nxt < total) issue(nxt, q1, g1, st1);
+    compute(cur, q0, g0, st0);
+    if (nxt >= total) break;
+    cur = nxt;
+    nxt = next_wanted(cur + 1);
+    wait_copies<0>();
+    ring_barrier();
+    if (nxt < total) issue(nxt, q0, g0, st0);
+    compute(cur, q1, g1, st1);
+    cur = nxt;
+  }
 
   if (!key_ok) return;
   // lane owns key my_key; register i of tile dt is d = 32 dt + acc_row(i)
+  if (role == 1) {
 #pragma unroll
-  for (int dt = 0; dt < D / 32; ++dt) dk[dt] *= p.scale;
+    for (int dt = 0; dt < D / 32; ++dt) acc[dt] *= p.scale;
+  }
   if (p.n_split > 1) {
-    // fp32 partial [split][b][key (over segments)][k_t][D], summed by attn_dkv_reduce
+    // fp32 partial [split][b][key (over segments)][k_t][D], dK then dV at +partial_half; summed by attn_dkv_reduce
     const int64_t key_index = static_cast<int64_t>(p.seg_key0[seg]) + my_key;
     const int64_t row = ((static_cast<int64_t>(split) * p.b + bi) * p.total_keys + key_index) * p.k_t + hk;
-    float* pk = p.dkv_partial + row * D;
-    float* pv = p.dkv_partial + p.partial_half + row * D;
+    float* pa = p.dkv_partial + (role == 1 ? 0 : p.partial_half) + row * D;
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
         const int d = dt * 32 + 8 * jj + rbase;
-        *reinterpret_cast<float4*>(pk + d) = make_float4(dk[dt][4 * jj], dk[dt][4 * jj + 1], dk[dt][4 * jj + 2],
-                                                         dk[dt][4 * jj + 3]);
-        *reinterpret_cast<float4*>(pv + d) = make_float4(dv[dt][4 * jj], dv[dt][4 * jj + 1], dv[dt][4 * jj + 2],
-                                                         dv[dt][4 * jj + 3]);
+        *reinterpret_cast<float4*>(pa + d) = make_float4(acc[dt][4 * jj], acc[dt][4 * jj + 1], acc[dt][4 * jj + 2],
+                                                         acc[dt][4 * jj + 3]);
       }
     return;
   }
   const int64_t off = bi * S.bstride + static_cast<int64_t>(my_key) * S.ld + hk * D;
   const int64_t doff = bi * S.d_bstride + static_cast<int64_t>(my_key) * S.d_ld + hk * D;
-  if (S.rk) {
+  const uint16_t* receipt = role == 1 ? S.rk : S.rv;
+  if (receipt) {
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
         const int d = dt * 32 + 8 * jj + rbase;
-        const u32x2 rk = *reinterpret_cast<const u32x2*>(S.rk + off + d);
-        const u32x2 rv = *reinterpret_cast<const u32x2*>(S.rv + off + d);
-        dk[dt][4 * jj] += lo16(rk[0]);
-        dk[dt][4 * jj + 1] += hi16(rk[0]);
-        dk[dt][4 * jj + 2] += lo16(rk[1]);
-        dk[dt][4 * jj + 3] += hi16(rk[1]);
-        dv[dt][4 * jj] += lo16(rv[0]);
-        dv[dt][4 * jj + 1] += hi16(rv[0]);
-        dv[dt][4 * jj + 2] += lo16(rv[1]);
-        dv[dt][4 * jj + 3] += hi16(rv[1]);
+        const u32x2 r = *reinterpret_cast<const u32x2*>(receipt + off + d);
+        acc[dt][4 * jj] += lo16(r[0]);
+        acc[dt][4 * jj + 1] += hi16(r[0]);
+        acc[dt][4 * jj + 2] += lo16(r[1]);
+        acc[dt][4 * jj + 3] += hi16(r[1]);
       }
   }
-  if (S.rope) {
+  if (role == 1 && S.rope) {
     constexpr int HALF_T = D / 64;
     const float2* tab = p.rope + static_cast<int64_t>(S.rope_row0 + my_key) * (D / 2);
 #pragma unroll
@@ -590,20 +692,19 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkdv_kernel(AttnParams p) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const float2 cs = tab[dt * 32 + acc_row(i, lane)];
-        const float a = dk[dt][i], b = dk[dt + HALF_T][i];
-        dk[dt][i] = a * cs.x + b * cs.y;              // rotate by -angle
-        dk[dt + HALF_T][i] = b * cs.x - a * cs.y;
+        const float a = acc[dt][i], b = acc[dt + HALF_T][i];
+        acc[dt][i] = a * cs.x + b * cs.y;              // rotate by -angle
+        acc[dt + HALF_T][i] = b * cs.x - a * cs.y;
       }
   }
+  uint16_t* dst = (role == 1 ? S.dk : S.dv) + doff;
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
       const int d = dt * 32 + 8 * jj + rbase;
-      *reinterpret_cast<u32x2*>(S.dk + doff + d) =
-          u32x2{pack2(dk[dt][4 * jj], dk[dt][4 * jj + 1]), pack2(dk[dt][4 * jj + 2], dk[dt][4 * jj + 3])};
-      *reinterpret_cast<u32x2*>(S.dv + doff + d) =
-          u32x2{pack2(dv[dt][4 * jj], dv[dt][4 * jj + 1]), pack2(dv[dt][4 * jj + 2], dv[dt][4 * jj + 3])};
+      *reinterpret_cast<u32x2*>(dst + d) =
+          u32x2{pack2(acc[dt][4 * jj], acc[dt][4 * jj + 1]), pack2(acc[dt][4 * jj + 2], acc[dt][4 * jj + 3])};
     }
 }
 
@@ -650,16 +751,22 @@ __global__ void __launch_bounds__(64) attn_dkv_reduce_kernel(AttnParams p) {
 }
 
 // ------------------------------------------------------------------ backward: dQ
-// grid: (q tiles of 128, a_t heads, b); 4 waves x 32 queries; loops over key tiles.
+// One workgroup per (128-query tile, query head, batch element), flat grid in
+// the forward's heaviest-first order; 4 waves x 32 queries.  Key tiles of 32
+// keep Q, dO, dQ and the two score tiles within 256 registers, so two
+// workgroups share a CU.  Per tile: S^T = K Q^T and dP^T = V dO^T, then
+// dS^T = P^T (dP^T - delta) feeds dQ^T += K^T dS^T from registers.
 template <int D>
-__global__ void __launch_bounds__(256, 1) attn_bwd_dq_kernel(AttnParams p) {
-  constexpr int TB = KT * D * 2;
-  __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB], k2[TB], v2[TB];
+__global__ void __launch_bounds__(256, 2) attn_bwd_dq_kernel(AttnParams p) {
+  constexpr int KQ = 32;                     // keys per tile
+  constexpr int TB = KQ * D * 2;
+  __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB];
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave: scalar code for wave-level decisions
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n_qt = (p.n_q + 127) / 128;
-  const int qt = n_qt - 1 - blockIdx.x;
-  const int hq = blockIdx.y, bi = blockIdx.z;
+  const int nh = p.a_t * p.b;
+  const int qt = n_qt - 1 - static_cast<int>(blockIdx.x) / nh;
+  const int hq = static_cast<int>(blockIdx.x) % nh % p.a_t, bi = static_cast<int>(blockIdx.x) % nh / p.a_t;
   const int hk = hq / (p.a_t / p.k_t);
   const int q_row0 = qt * 128;
   const int my_q = q_row0 + wave * 32 + (lane & 31);
@@ -687,70 +794,45 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dq_kernel(AttnParams p) {
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) dq[i] = f32x16{};
 
-  const int ntiles = total_tiles(p, KT);
   auto issue = [&](int seg, int t0, uint8_t* kt, uint8_t* vt) __attribute__((always_inline)) {
     const KvSeg& s = p.seg[seg];
     const int64_t off = bi * s.bstride + static_cast<int64_t>(t0) * s.ld + hk * D;
-    tile_load<D, KT>(kt, s.k + off, s.ld, s.n - t0, wave, lane);
-    tile_load<D, KT>(vt, s.v + off, s.ld, s.n - t0, wave, lane);
+    tile_load<D, KQ>(kt, s.k + off, s.ld, s.n - t0, wave, lane);
+    tile_load<D, KQ>(vt, s.v + off, s.ld, s.n - t0, wave, lane);
   };
   auto compute = [&](int seg, int t0, const uint8_t* kt, const uint8_t* vt) __attribute__((always_inline)) {
-    const KvSeg& s = p.seg[seg];
-    const int kpos0 = s.pos0 + t0;
-    const int kvalid = min(KT, s.n - t0);
-    f32x16 sc[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
+    const int kpos0 = p.seg[seg].pos0 + t0;
+    const int kvalid = min(KQ, p.seg[seg].n - t0);
+    f32x16 sc = f32x16{}, dp = f32x16{};
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk)
+    for (int kk = 0; kk < D / 16; ++kk) {
+      sc = mfma(frag_rows<D>(kt, 0, kk, lane), qf[kk], sc);
+      dp = mfma(frag_rows<D>(vt, 0, kk, lane), dof[kk], dp);
+    }
+    if (kpos0 + KQ - 1 > pos_min || kvalid < KQ) {      // tile straddles the diagonal (or is ragged)
+      const int lim = (q_ok ? min(my_pos - kpos0, kvalid - 1) : -1) - rbase;
 #pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) {
-        sc[t2] = mfma(frag_rows<D>(kt, t2 * 32, kk, lane), qf[kk], sc[t2]);
-        dp[t2] = mfma(frag_rows<D>(vt, t2 * 32, kk, lane), dof[kk], dp[t2]);
-      }
-    const bool masked = kpos0 + KT - 1 > pos_min || kvalid < KT;
-    const int lim = q_ok ? min(my_pos - kpos0, kvalid - 1) : -1;
+      for (int i = 0; i < 16; ++i)
+        if (8 * (i >> 2) + (i & 3) > lim) sc[i] = -INFINITY;
+    }
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2)
+    for (int i = 0; i < 16; ++i) sc[i] = fast_exp2(fmaf(sc[i], c, -my_lse)) * (dp[i] - my_delta);   // dS^T
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float pr = fast_exp2(fmaf(sc[t2][i], c, -my_lse));
-        if (masked && t2 * 32 + 8 * (i >> 2) + rbase + (i & 3) > lim) pr = 0.f;
-        sc[t2][i] = pr * (dp[t2][i] - my_delta);            // dS^T
-      }
+    for (int g = 0; g < 2; ++g) {
+      const bf16x8 sf = frag_acc(sc, 8 * g);
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-      for (int g = 0; g < 2; ++g) {
-        const bf16x8 sf = frag_acc(sc[t2], 8 * g);
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) dq[dt] = mfma(frag_cols<D>(kt, dt, t2 * 2 + g, lane), sf, dq[dt]);
-      }
+      for (int dt = 0; dt < D / 32; ++dt) dq[dt] = mfma(frag_cols<D>(kt, dt, g, lane), sf, dq[dt]);
+    }
   };
-
-  auto kbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
-    if constexpr (decltype(b)::value == 0) return k0;
-    else if constexpr (decltype(b)::value == 1) return k1;
-    else return k2;
-  };
-  auto vbuf = [&](auto b) __attribute__((always_inline)) -> uint8_t* {
-    if constexpr (decltype(b)::value == 0) return v0;
-    else if constexpr (decltype(b)::value == 1) return v1;
-    else return v2;
-  };
-  run_ring<KT * D / 1024>(
-      ntiles,
-      [&](int from) __attribute__((always_inline)) {
-        int s_, t_;
-        return next_key_tile(p, from, ntiles, pos_max, s_, t_);
+  run_ring2(
+      p, pos_max, KQ,
+      [&](int seg, int t0, auto b) __attribute__((always_inline)) {
+        if constexpr (decltype(b)::value == 0) issue(seg, t0, k0, v0);
+        else issue(seg, t0, k1, v1);
       },
-      [&](int t, auto b) __attribute__((always_inline)) {
-        int s_, t_;
-        find_tile(p, t, KT, s_, t_);
-        issue(s_, t_, kbuf(b), vbuf(b));
-      },
-      [&](int t, auto b) __attribute__((always_inline)) {
-        int s_, t_;
-        find_tile(p, t, KT, s_, t_);
-        compute(s_, t_, kbuf(b), vbuf(b));
+      [&](int seg, int t0, auto b) __attribute__((always_inline)) {
+        if constexpr (decltype(b)::value == 0) compute(seg, t0, k0, v0);
+        else compute(seg, t0, k1, v1);
       });
 
   if (!q_ok) return;
@@ -795,13 +877,14 @@ hipError_t bwd_impl(const AttnParams& p, int part, hipStream_t stream) {
     const int64_t rows = static_cast<int64_t>(p.b) * p.n_q;
     hipLaunchKernelGGL(attn_delta_kernel<D>, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, p);
   } else if (part == 1) {
-    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(count_blocks(p, 128), p.k_t * p.n_split, p.b), dim3(256), 0,
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(count_blocks(p, 128), p.k_t * p.n_split, p.b), dim3(512), 0,
                        stream, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.n_split == 1) return e;
     hipLaunchKernelGGL(attn_dkv_reduce_kernel<D>, dim3(p.total_keys, p.k_t, p.b), dim3(64), 0, stream, p);
   } else {
-    hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3((p.n_q + 127) / 128, p.a_t, p.b), dim3(256), 0, stream, p);
+    const unsigned blocks = static_cast<unsigned>((p.n_q + 127) / 128) * p.a_t * p.b;
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3(blocks), dim3(256), 0, stream, p);
   }
   return hipGetLastError();
 }
