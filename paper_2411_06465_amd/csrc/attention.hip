@@ -39,6 +39,8 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 #define GPTR(p) ((const __attribute__((address_space(1))) void*)(p))
 #define LPTR(p) ((__attribute__((address_space(3))) void*)(p))
@@ -47,10 +49,13 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int KT = 64;            // keys per tile (forward, dQ)
 constexpr int QT = 64;            // queries per tile (dK/dV)
+// LDS fragment reads kept in flight ahead of the products, per kernel
+constexpr int kLookFwd = 6, kLookDq = 4, kLookDkv = 4;
 
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+// Two floats to a packed bf16 pair with one conversion (round to nearest even).
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
-  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
 __device__ __forceinline__ float lo16(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float hi16(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
@@ -72,20 +77,28 @@ __device__ __forceinline__ void ring_barrier() {
 
 // ------------------------------------------------------------------ LDS tiles
 // Row-major [rows][D] bf16 tile; 16-byte chunk c of row r sits at chunk c ^ swz(r).
+// The LDS serves 256 bytes (64 banks) per cycle.  Two read patterns must be
+// conflict-free: a row fragment (16 lanes, 16 consecutive rows, one chunk
+// each) needs swz to be a permutation over every aligned block of 16 rows; a
+// transposing column fragment (32 lanes, 4 consecutive rows x an aligned group
+// of 4 chunks) needs the 4 rows to map that group to 4 different groups, i.e.
+// distinct swz >> 2 across 4 consecutive rows.  At D = 64 a row is half a
+// bank line, so row parity picks the half and swz only has to separate rows
+// of equal parity.  Also swz(r + 8) = swz(r) ^ 4: a column fragment reads
+// rows r and r + 8, and the second address is then the first address of the
+// neighbouring 32-column block plus a constant, so no extra register holds it.
 template <int D>
 __device__ __forceinline__ int swz(int row) {
-  return D == 128 ? ((row & 7) << 1) : (row & 7);
-}
-template <int D>
-__device__ __forceinline__ int t_off(int row, int chunk) {
-  return row * (D * 2) + ((chunk ^ swz<D>(row)) << 4);
+  const int b1 = (row >> 1) & 1, b2 = (row >> 2) & 1, b3 = (row >> 3) & 1;
+  return D == 128 ? ((((row & 3) ^ b3) << 2) | (b2 << 1) | (row & 1)) : (((b1 ^ b3) << 2) | (b2 << 1) | b1);
 }
 
 // Copy rows [0, ROWS) of src (row stride ld, rows >= n_valid clamped to the
 // last valid row) into an LDS tile; the NW waves of the block share the work.
 // A copy instruction moves RPK whole rows (1 KB); lane i lands at byte 16 i of
-// the instruction's LDS chunk.  The wave's copies all start at rows of the same
-// parity, so each lane's swizzled source column is fixed: a buffer load with
+// the instruction's LDS chunk.  The wave's copies start at rows that agree
+// modulo 4 * RPK (the waves take every NW-th chunk, NW a multiple of 4), which
+// fixes swz, so each lane's swizzled source column is fixed: a buffer load with
 // the tile base in the (uniform) resource, the row block in the scalar offset
 // and one 32-bit per-lane offset, except on a ragged tail.
 constexpr int kBufferDword3 = 0x00020000;    // raw buffer, 32-bit data format (gfx9 family)
@@ -99,7 +112,7 @@ __device__ __forceinline__ void tile_load(uint8_t* lds, const uint16_t* src, int
   const __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(src), 0, -1, kBufferDword3);
   const int lrow = lane / CH;
-  const int lc = (lane % CH) ^ swz<D>(wave * RPK + lrow);   // row parity of every copy of this wave
+  const int lc = (lane % CH) ^ swz<D>(wave * RPK + lrow);   // the same for every copy of this wave
   const int ldb = static_cast<int>(ld) * 2;                 // row stride in bytes
   if (n_valid >= ROWS) {
     const uint32_t lane_off = static_cast<uint32_t>(lrow * ldb + lc * 16);
@@ -119,27 +132,41 @@ __device__ __forceinline__ void tile_load(uint8_t* lds, const uint16_t* src, int
   }
 }
 
-// MFMA operand with the tile's rows as its 32 rows: rows row0 + lane%32,
-// contraction chunk 2*kk + lane/32 (d = 16 kk + 8 (lane/32) + 0..7).
+// Per-lane LDS byte offsets of the two fragment shapes below, at kk = 0 and
+// dt = 0 of a tile's first row block.  With swz periodic in 16 rows, the
+// other kk / dt are an XOR of the low byte (the 16-byte chunk within a row),
+// and other row blocks a constant: one register per shape.
+struct LaneAddr {
+  int rows;   // row fragment: row lane%32, chunk lane/32
+  int cols;   // column fragment: row 4 (lane/32) + (lane%16)/4, column 16 ((lane/16)%2) + 4 (lane%4)
+};
 template <int D>
-__device__ __forceinline__ bf16x8 frag_rows(const uint8_t* lds, int row0, int kk, int lane) {
-  return *reinterpret_cast<const bf16x8*>(lds + t_off<D>(row0 + (lane & 31), 2 * kk + (lane >> 5)));
+__device__ __forceinline__ LaneAddr lane_addr(int lane) {
+  const int h = lane >> 5, li = lane & 15;
+  const int rr = lane & 31;
+  const int cr = 4 * h + (li >> 2);
+  const int low = 2 * ((lane >> 4) & 1) + ((li & 3) >> 1);   // chunk within the 4-chunk group
+  return LaneAddr{rr * (D * 2) + ((swz<D>(rr) ^ h) << 4),
+                  cr * (D * 2) + ((low ^ swz<D>(cr)) << 4) + ((li & 1) << 3)};
+}
+// MFMA operand with the tile's rows as its 32 rows: rows row0 + lane%32 (row0
+// a multiple of 16), contraction chunk 2*kk + lane/32 (d = 16 kk + 8 (lane/32) + 0..7).
+template <int D>
+__device__ __forceinline__ bf16x8 frag_rows(const uint8_t* lds, int row0, int kk, LaneAddr la) {
+  return *reinterpret_cast<const bf16x8*>(lds + row0 * (D * 2) + (la.rows ^ (kk << 5)));
 }
 // MFMA operand with the tile's columns as its rows: d = 32 dt + lane%32; its 8
 // contraction slots are tile rows 16 g16 + {4h .. 4h+3, 8+4h .. 8+4h+3},
 // h = lane/32 -- the same order in which a lane holds accumulator rows of a
-// 32x32 MFMA (see frag_acc).  Two transposing 64-bit LDS reads.
+// 32x32 MFMA (see frag_acc).  Two transposing 64-bit LDS reads; rows r + 8
+// have swz(r) ^ 4, which is the XOR pattern of column block dt ^ 1.
 template <int D>
-__device__ __forceinline__ bf16x8 frag_cols(const uint8_t* lds, int dt, int g16, int lane) {
-  const int li = lane & 15;
-  const int row = 16 * g16 + 4 * (lane >> 5) + (li >> 2);
-  const int d = 32 * dt + 16 * ((lane >> 4) & 1) + 4 * (li & 3);
-  const int off = t_off<D>(row, d >> 3) + ((d & 7) << 1);
-  const int off8 = t_off<D>(row + 8, d >> 3) + ((d & 7) << 1);
-  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      reinterpret_cast<__attribute__((address_space(3))) i16x4*>(LPTR(const_cast<uint8_t*>(lds) + off)));
-  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      reinterpret_cast<__attribute__((address_space(3))) i16x4*>(LPTR(const_cast<uint8_t*>(lds) + off8)));
+__device__ __forceinline__ bf16x8 frag_cols(const uint8_t* lds, int dt, int g16, LaneAddr la) {
+  const uint8_t* base = lds + g16 * 16 * (D * 2);
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<__attribute__((address_space(3))) i16x4*>(
+      LPTR(const_cast<uint8_t*>(base) + (la.cols ^ (dt << 6)))));
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<__attribute__((address_space(3))) i16x4*>(
+      LPTR(const_cast<uint8_t*>(base) + 8 * (D * 2) + (la.cols ^ ((dt ^ 1) << 6)))));
   return __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, a)[0], __builtin_bit_cast(u32x2, a)[1],
                                           __builtin_bit_cast(u32x2, b)[0], __builtin_bit_cast(u32x2, b)[1]});
 }
@@ -290,7 +317,7 @@ __device__ __forceinline__ void run_ring2(const AttnParams& p, int pos_max, int 
 }
 
 template <int D>
-__global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) attn_fwd_kernel(AttnParams p) {
   constexpr int TB = KT * D * 2;
   __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -307,6 +334,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
   const int blk_last = min(q_row0 + 127, p.n_q - 1);
   const int pos_min = qpos(p.qmap, q_row0), pos_max = qpos(p.qmap, blk_last);
   const int rbase = 4 * (lane >> 5);
+  const LaneAddr la = lane_addr<D>(lane);
 
   bf16x8 qf[D / 16];
   {
@@ -330,10 +358,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
     const int kpos0 = p.seg[seg].pos0 + t0;
     const int kvalid = min(KT, p.seg[seg].n - t0);
     f32x16 sc[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk)
-#pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) sc[t2] = mfma(frag_rows<D>(kt, t2 * 32, kk, lane), qf[kk], sc[t2]);
+    scores2<D, kLookFwd>(kt, 0, qf, sc[0], kt, 32, qf, sc[1], la);
     if (kpos0 + KT - 1 > pos_min || kvalid < KT) {       // tile straddles the diagonal (or is ragged)
       // last visible key row for this query, relative to the lane's first row
       const int lim = min(my_pos - kpos0, kvalid - 1) - rbase;
@@ -343,11 +368,11 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
         for (int i = 0; i < 16; ++i)
           if (t2 * 32 + 8 * (i >> 2) + (i & 3) > lim) sc[t2][i] = -INFINITY;
     }
-    float mx = fmaxf(sc[0][0], sc[0][1]);
+    float mx = __builtin_fmaxf(sc[0][0], sc[0][1]);           // a chain of three-input maxima
 #pragma unroll
-    for (int i = 2; i < 16; i += 2) mx = fmaxf(mx, fmaxf(sc[0][i], sc[0][i + 1]));
+    for (int i = 2; i < 16; i += 2) mx = __builtin_fmaxf(__builtin_fmaxf(mx, sc[0][i]), sc[0][i + 1]);
 #pragma unroll
-    for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(sc[1][i], sc[1][i + 1]));
+    for (int i = 0; i < 16; i += 2) mx = __builtin_fmaxf(__builtin_fmaxf(mx, sc[1][i]), sc[1][i + 1]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
     if (__builtin_amdgcn_ballot_w64(mx > m_run)) {
       const float m_new = fmaxf(m_run, mx);
@@ -368,14 +393,10 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnParams p) {
         rs += pr;
       }
     l_run += rs;
+    bf16x8 pf[4];
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-      for (int g = 0; g < 2; ++g) {
-        const bf16x8 pf = frag_acc(sc[t2], 8 * g);
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) o[dt] = mfma(frag_cols<D>(vt, dt, t2 * 2 + g, lane), pf, o[dt]);
-      }
+    for (int g = 0; g < 4; ++g) pf[g] = frag_acc(sc[g >> 1], 8 * (g & 1));
+    accum_t<D, 4, kLookFwd>(vt, pf, o, la);
   };
 
   run_ring2(
@@ -434,41 +455,50 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(AttnParams p) {
   }
 }
 
-// s[h] += A[32 h + (0..31)] x^T over the tile's D columns, with A the LDS
-// tile and x the lane's 32 key rows (K or V) in registers: S^T or dP^T for 64
-// queries.  The schedule keeps two fragment reads ahead of the products, so
-// at most three fragments are live instead of all sixteen.
-template <int D>
-__device__ __forceinline__ void scores_t(const uint8_t* lds, const bf16x8 (&x)[D / 16], f32x16 (&s)[2], int lane) {
+// ------------------------------------------------------------------ pipelined products
+// Two accumulator chains over the D columns of LDS tiles, with the B operands
+// in registers:  s0 += A0[r0 + (0..31)] x0^T,  s1 += A1[r1 + (0..31)] x1^T.
+// The schedule keeps LA fragment reads in flight ahead of the products
+// (without it the compiler reads each fragment right before its product and
+// the LDS latency is exposed on every step).
+template <int D, int LA>
+__device__ __forceinline__ void scores2(const uint8_t* a0, int r0, const bf16x8 (&x0)[D / 16], f32x16& s0,
+                                        const uint8_t* a1, int r1, const bf16x8 (&x1)[D / 16], f32x16& s1,
+                                        LaneAddr la) {
+  constexpr int N = D / 8;               // products (and fragment reads)
+  constexpr int L = LA < N ? LA : N - 1;
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk)
+  for (int kk = 0; kk < D / 16; ++kk) {
+    s0 = mfma(frag_rows<D>(a0, r0, kk, la), x0[kk], s0);
+    s1 = mfma(frag_rows<D>(a1, r1, kk, la), x1[kk], s1);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x100, L, 0);      // LDS reads
 #pragma unroll
-    for (int h = 0; h < 2; ++h) s[h] = mfma(frag_rows<D>(lds, 32 * h, kk, lane), x[kk], s[h]);
-  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);      // LDS reads
-#pragma unroll
-  for (int i = 0; i < D / 8 - 2; ++i) {
+  for (int i = 0; i < N - L; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, L, 0);
 }
 
-// acc[dt] += A^T x over 64 queries: A the LDS tile read transposed (d rows,
-// query contraction) and x[g] the bf16 P^T or dS^T of query group g from
-// registers: dV^T or dK^T.  Two fragment reads stay ahead of the products.
-template <int D>
-__device__ __forceinline__ void accum_t(const uint8_t* lds, const bf16x8 (&x)[4], f32x16 (&acc)[D / 32], int lane) {
+// acc[dt] += A^T x over NG groups of 16 rows: A the LDS tile read transposed
+// (d rows, row-index contraction), x[g] a bf16 operand from registers (P^T,
+// dS^T); two reads per fragment, LA fragments in flight.
+template <int D, int NG, int LA>
+__device__ __forceinline__ void accum_t(const uint8_t* lds, const bf16x8 (&x)[NG], f32x16 (&acc)[D / 32], LaneAddr la) {
+  constexpr int N = NG * D / 32;
+  constexpr int L = LA < N ? LA : N - 1;
 #pragma unroll
-  for (int g = 0; g < 4; ++g)
+  for (int g = 0; g < NG; ++g)
 #pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) acc[dt] = mfma(frag_cols<D>(lds, dt, g, lane), x[g], acc[dt]);
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);      // LDS reads (two per fragment)
+    for (int dt = 0; dt < D / 32; ++dt) acc[dt] = mfma(frag_cols<D>(lds, dt, g, la), x[g], acc[dt]);
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * L, 0);
 #pragma unroll
-  for (int i = 0; i < D / 8 - 2; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
+  for (int i = 0; i < N - L; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, L, 0);
 }
 
 // ------------------------------------------------------------------ backward: dK, dV
@@ -486,11 +516,11 @@ __device__ __forceinline__ void accum_t(const uint8_t* lds, const bf16x8 (&x)[4]
 // (softmax on one, products on the other) that interleave.  Both use the same
 // bf16 P^T, the one dV is built from.
 template <int D>
-__global__ void __launch_bounds__(512, 2) attn_bwd_dkdv_kernel(AttnParams p) {
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) attn_bwd_dkdv_kernel(AttnParams p) {
   constexpr int TB = QT * D * 2;
   // Two stages of Q and dO tiles (64 KB at D = 128: every tile offset fits a
   // ds_read immediate), then the statistics and the P^T handover.
-  __shared__ __attribute__((aligned(16))) uint8_t q0[TB], g0[TB], q1[TB], g1[TB];   // Q, dO tiles
+  __shared__ __attribute__((aligned(16))) uint8_t qg0[2][TB], qg1[2][TB];   // per stage: Q tile, then dO tile
   __shared__ __attribute__((aligned(16))) float st0[2][QT], st1[2][QT];             // lse, delta
   __shared__ __attribute__((aligned(16))) u32x4 xp[4][QT / 16][64];    // P^T handover: [group][16 queries][lane]
   const int tid = threadIdx.x, lane = tid & 63;
@@ -509,6 +539,11 @@ __global__ void __launch_bounds__(512, 2) attn_bwd_dkdv_kernel(AttnParams p) {
   const int grp_kpos0 = S.pos0 + k0 + grp * 32;
   const int blk_kpos0 = S.pos0 + k0;
   const int rbase = 4 * (lane >> 5);
+  const LaneAddr la = lane_addr<D>(lane);
+  // Offsets into a stage's [Q | dO] pair: the first product reads Q (role 0)
+  // or dO (role 1), the second reads dO (role 0) or Q (role 1).
+  const LaneAddr la1{la.rows + role * TB, la.cols};
+  const LaneAddr la2{la.rows, la.cols + (1 - role) * TB};
 
   bf16x8 kv[D / 16];                     // role 0: K rows, role 1: V rows of the group's keys
   {
@@ -551,13 +586,18 @@ __global__ void __launch_bounds__(512, 2) attn_bwd_dkdv_kernel(AttnParams p) {
     const int qr0 = qt * QT;
     const int qlast = min(qr0 + QT - 1, p.n_q - 1);
     const int qp0 = qpos(p.qmap, qr0), qpl = qpos(p.qmap, qlast);
-    const bool active = qpl >= grp_kpos0;              // some query of the tile sees a key of the group
+    // Every group works on every tile the block visits; on the one or two
+    // diagonal tiles where all of a group's keys follow every query, the
+    // causal mask zeroes its P^T (a skip there would cost register copies at
+    // the branch joins on every tile).
     const bool full = qp0 >= grp_kpos0 + 31 && qlast == qr0 + QT - 1 && qpl - qp0 == QT - 1;
     const bool contiguous = qpl - qp0 == qlast - qr0;
+    // Both roles run one instruction stream over role-selected tiles (role 0:
+    // S^T from Q, dV^T from dO; role 1: dP^T from dO, dK^T from Q), so the
+    // accumulators never meet at a branch join.
     f32x16 s[2] = {f32x16{}, f32x16{}};              // role 0: S^T -> P^T, role 1: dP^T -> dS^T
-    if (active) {
-      if (role == 0) scores_t<D>(qt_l, kv, s, lane);
-      else scores_t<D>(gt_l, kv, s, lane);
+    scores2<D, kLookDkv>(qt_l, 0, kv, s[0], qt_l, 32, kv, s[1], la1);
+    {
       if (role == 0) {
 #pragma unroll
         for (int h = 0; h < 2; ++h)
@@ -596,16 +636,11 @@ __global__ void __launch_bounds__(512, 2) attn_bwd_dkdv_kernel(AttnParams p) {
       }
     }
     ring_barrier();                                    // P^T of every group is visible to its partner
-    if (!active) return;
+    bf16x8 x[4];                                       // role 0: P^T, role 1: dS^T (bf16)
     if (role == 0) {
-      bf16x8 pf[4];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) pf[g] = __builtin_bit_cast(bf16x8, xp[grp][g][lane]);
-      __builtin_amdgcn_sched_barrier(0);
-      accum_t<D>(gt_l, pf, acc, lane);
+      for (int g = 0; g < 4; ++g) x[g] = __builtin_bit_cast(bf16x8, xp[grp][g][lane]);
     } else {
-      // dS^T for all four query groups first, so dP^T is dead before the products start
-      bf16x8 sf[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const u32x4 pp = xp[grp][g][lane];
@@ -619,31 +654,31 @@ __global__ void __launch_bounds__(512, 2) attn_bwd_dkdv_kernel(AttnParams p) {
           ds[2 * j] = lo16(pp[j]) * (s[h][i0 + 2 * j] - dev[2 * j]);
           ds[2 * j + 1] = hi16(pp[j]) * (s[h][i0 + 2 * j + 1] - dev[2 * j + 1]);
         }
-        sf[g] = __builtin_bit_cast(
+        x[g] = __builtin_bit_cast(
             bf16x8, u32x4{pack2(ds[0], ds[1]), pack2(ds[2], ds[3]), pack2(ds[4], ds[5]), pack2(ds[6], ds[7])});
       }
-      __builtin_amdgcn_sched_barrier(0);
-      accum_t<D>(qt_l, sf, acc, lane);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    accum_t<D, 4, kLookDkv>(qt_l, x, acc, la2);
   };
 
   // Two-stage ring over the query tiles: tile j is used from one buffer set
   // while tile j + 1 lands in the other.
   int cur = next_wanted(0);
-  if (cur < total) issue(cur, q0, g0, st0);
+  if (cur < total) issue(cur, qg0[0], qg0[1], st0);
   while (cur < total) {
     int nxt = next_wanted(cur + 1);
     wait_copies<0>();
     ring_barrier();                      // tile cur is visible; the other buffers are free
-    if (nxt < total) issue(nxt, q1, g1, st1);
-    compute(cur, q0, g0, st0);
+    if (nxt < total) issue(nxt, qg1[0], qg1[1], st1);
+    compute(cur, qg0[0], qg0[1], st0);
     if (nxt >= total) break;
     cur = nxt;
     nxt = next_wanted(cur + 1);
     wait_copies<0>();
     ring_barrier();
-    if (nxt < total) issue(nxt, q0, g0, st0);
-    compute(cur, q1, g1, st1);
+    if (nxt < total) issue(nxt, qg0[0], qg0[1], st0);
+    compute(cur, qg1[0], qg1[1], st1);
     cur = nxt;
   }
 
@@ -757,7 +792,7 @@ __global__ void __launch_bounds__(64) attn_dkv_reduce_kernel(AttnParams p) {
 // workgroups share a CU.  Per tile: S^T = K Q^T and dP^T = V dO^T, then
 // dS^T = P^T (dP^T - delta) feeds dQ^T += K^T dS^T from registers.
 template <int D>
-__global__ void __launch_bounds__(256, 2) attn_bwd_dq_kernel(AttnParams p) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) attn_bwd_dq_kernel(AttnParams p) {
   constexpr int KQ = 32;                     // keys per tile
   constexpr int TB = KQ * D * 2;
   __shared__ __attribute__((aligned(16))) uint8_t k0[TB], v0[TB], k1[TB], v1[TB];
@@ -775,6 +810,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq_kernel(AttnParams p) {
   const int blk_last = min(q_row0 + 127, p.n_q - 1);
   const int pos_min = qpos(p.qmap, q_row0), pos_max = qpos(p.qmap, blk_last);
   const int rbase = 4 * (lane >> 5);
+  const LaneAddr la = lane_addr<D>(lane);
 
   bf16x8 qf[D / 16], dof[D / 16];
   {
@@ -804,11 +840,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq_kernel(AttnParams p) {
     const int kpos0 = p.seg[seg].pos0 + t0;
     const int kvalid = min(KQ, p.seg[seg].n - t0);
     f32x16 sc = f32x16{}, dp = f32x16{};
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-      sc = mfma(frag_rows<D>(kt, 0, kk, lane), qf[kk], sc);
-      dp = mfma(frag_rows<D>(vt, 0, kk, lane), dof[kk], dp);
-    }
+    scores2<D, kLookDq>(kt, 0, qf, sc, vt, 0, dof, dp, la);
     if (kpos0 + KQ - 1 > pos_min || kvalid < KQ) {      // tile straddles the diagonal (or is ragged)
       const int lim = (q_ok ? min(my_pos - kpos0, kvalid - 1) : -1) - rbase;
 #pragma unroll
@@ -817,12 +849,8 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq_kernel(AttnParams p) {
     }
 #pragma unroll
     for (int i = 0; i < 16; ++i) sc[i] = fast_exp2(fmaf(sc[i], c, -my_lse)) * (dp[i] - my_delta);   // dS^T
-#pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      const bf16x8 sf = frag_acc(sc, 8 * g);
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) dq[dt] = mfma(frag_cols<D>(kt, dt, g, lane), sf, dq[dt]);
-    }
+    const bf16x8 sf[2] = {frag_acc(sc, 0), frag_acc(sc, 8)};
+    accum_t<D, 2, kLookDq>(kt, sf, dq, la);
   };
   run_ring2(
       p, pos_max, KQ,
