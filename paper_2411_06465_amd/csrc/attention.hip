@@ -217,43 +217,6 @@ __device__ __forceinline__ int next_key_tile(const AttnParams& p, int from, int 
 }
 
 
-// Three-stage copy ring over a sequence of work items (key or query tiles):
-// item k lives in buffer k % 3; while item k is computed the copies of items
-// k+1 and k+2 are in flight.  `next(i)` is the first wanted item at or after
-// i (`total` when none), `issue(item, buffer)` starts its copies (NC
-// instructions per wave, the same count for every item) and
-// `compute(item, buffer)` uses it.  Buffer b is passed as the constant
-// std::integral_constant<int, b>, so every LDS object is named statically and
-// the compiler sees that the reads of one buffer do not depend on the copies
-// landing in the others.
-template <int NC, class Next, class Issue, class Compute>
-__device__ __forceinline__ void run_ring(int total, Next next, Issue issue, Compute compute) {
-  using B0 = std::integral_constant<int, 0>;
-  using B1 = std::integral_constant<int, 1>;
-  using B2 = std::integral_constant<int, 2>;
-  int c0 = next(0);
-  int c1 = c0 < total ? next(c0 + 1) : total;
-  if (c0 < total) issue(c0, B0{});
-  if (c1 < total) issue(c1, B1{});
-  auto step = [&](auto cur_buf, auto far_buf) __attribute__((always_inline)) {
-    if (c1 < total) wait_copies<NC>();     // item c0 has landed; c1 may still be in flight
-    else wait_copies<0>();
-    ring_barrier();                        // every wave's copy of c0 is visible; the buffer of c0-1 is free
-    const int c2 = c1 < total ? next(c1 + 1) : total;
-    if (c2 < total) issue(c2, far_buf);
-    compute(c0, cur_buf);
-    c0 = c1;
-    c1 = c2;
-  };
-  while (c0 < total) {
-    step(B0{}, B2{});
-    if (c0 >= total) break;
-    step(B1{}, B0{});
-    if (c0 >= total) break;
-    step(B2{}, B1{});
-  }
-}
-
 // ------------------------------------------------------------------ forward
 // One workgroup per (128-query tile, query head, batch element); 4 waves x 32
 // queries, each lane holding one query's scores (S^T = K Q^T).  The launch is
@@ -299,6 +262,7 @@ __device__ __forceinline__ void run_ring2(const AttnParams& p, int pos_max, int 
     wait_copies<0>();
     ring_barrier();                      // every wave's copy is visible; the other buffer is free
     if (more) issue(ns, nt, B1{});
+    __builtin_amdgcn_sched_barrier(0);   // the copies go out now, not next to the wait for them
     compute(cs, ct, B0{});
     if (!more) break;
     cs = ns;
@@ -309,6 +273,7 @@ __device__ __forceinline__ void run_ring2(const AttnParams& p, int pos_max, int 
     wait_copies<0>();
     ring_barrier();
     if (more) issue(ns, nt, B0{});
+    __builtin_amdgcn_sched_barrier(0);
     compute(cs, ct, B1{});
     have = more;
     cs = ns;
@@ -671,6 +636,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     wait_copies<0>();
     ring_barrier();                      // tile cur is visible; the other buffers are free
     if (nxt < total) issue(nxt, qg1[0], qg1[1], st1);
+    __builtin_amdgcn_sched_barrier(0);   // the copies go out now, not next to the wait for them
     compute(cur, qg0[0], qg0[1], st0);
     if (nxt >= total) break;
     cur = nxt;
@@ -678,6 +644,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     wait_copies<0>();
     ring_barrier();
     if (nxt < total) issue(nxt, qg0[0], qg0[1], st0);
+    __builtin_amdgcn_sched_barrier(0);
     compute(cur, qg1[0], qg1[1], st1);
     cur = nxt;
   }

@@ -20,8 +20,8 @@
 //
 // Operand layouts: "KC" (reduction index contiguous: activations in the
 // forward, the output gradient in dX) is stored row by row, the 16-byte chunks
-// of a row permuted by an XOR with low row bits so that the 8 rows an 8-lane
-// group of a fragment read touches cover all 32 banks.  "MN" (reduction
+// of a row permuted by an XOR with row bits so that the 16 rows a 16-lane
+// group of a fragment read touches cover all 64 banks (256 bytes) once.  "MN" (reduction
 // index strided: the weight in dX, both operands of dW) is stored as k-rows
 // of 256 columns with the 16-byte chunks XOR-swizzled by row, and read with
 // two ds_read_b64_tr_b16 that hand each lane 4 consecutive k of one column --
@@ -78,17 +78,21 @@ __device__ __forceinline__ int xcd_remap(int bid, int nwg) {
 
 // ------------------------------------------------------------------ LDS layouts
 // KC tile: row r (0..255) holds its 32 k (64 bytes) at r*64, the four 16-byte
-// chunks permuted by c ^ ((r >> 1) & 3): the 8 rows one 8-lane group of a
-// fragment read touches then cover all 32 banks once.
-__device__ __forceinline__ int kc_off(int row, int chunk) { return row * 64 + ((chunk ^ ((row >> 1) & 3)) << 4); }
-// MN tile: k-row r (0..31), 16-byte chunk c (0..31) of its 256 columns.
-__device__ __forceinline__ int mn_swz(int row) { return (row & 3) << 1; }
+// chunks permuted by c ^ ((r >> 2) & 3).  Four rows share a 256-byte bank line
+// (r % 4 picks the quarter), so the 16 rows one 16-lane group of a fragment
+// read touches cover all 64 banks once.
+__device__ __forceinline__ int kc_off(int row, int chunk) { return row * 64 + ((chunk ^ ((row >> 2) & 3)) << 4); }
+// MN tile: k-row r (0..31), 16-byte chunk c (0..31) of its 256 columns,
+// stored at chunk c ^ 4 (r % 4).  A transposing read (32 lanes: 4 k-rows x an
+// aligned group of 4 chunks) then touches 4 different chunk groups, all 64
+// banks once; k-rows r and r + 4 share the pattern.
+__device__ __forceinline__ int mn_swz(int row) { return (row & 3) << 2; }
 __device__ __forceinline__ int mn_off(int row, int chunk) { return row * 512 + ((chunk ^ mn_swz(row)) << 4); }
 
 // Each stage holds 16 KB per operand; wave w copies LDS KB numbers
 // kb = w + WAVES * q.  KC: KB kb holds tile rows 16 kb + lane/4, 64 contiguous
 // bytes of each row per instruction (4 lanes), lane l fetching the chunk
-// that belongs at its LDS slot l % 4: chunk (l & 3) ^ ((l >> 3) & 3), the
+// that belongs at its LDS slot l % 4: chunk (l & 3) ^ ((l >> 4) & 3), the
 // same for every q.  A lane's source rows are fixed over K and kept as
 // pointers.  MN: KB kb holds k-rows 2 kb + lane/32.
 template <int WAVES>
@@ -100,7 +104,7 @@ struct KcRows {
 template <int WAVES>
 __device__ __forceinline__ KcRows<WAVES> kc_rows(const Operand& op, int x0, int tile_idx, int wave, int lane) {
   KcRows<WAVES> r;
-  r.c8 = 8 * ((lane & 3) ^ ((lane >> 3) & 3));
+  r.c8 = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
 #pragma unroll
   for (int q = 0; q < 16 / WAVES; ++q) {
     const int xr = 16 * (wave + WAVES * q) + (lane >> 2);
@@ -466,6 +470,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bk32(GemmParams p) {
     else wait_vm<0>();
     stage_barrier();
     if (kt + 3 < nk) issue((kt + 3) * BK, na, nb);
+    __builtin_amdgcn_sched_barrier(0);   // the copies go out now, not next to the wait for them
     compute(kt * BK, la, lb);
   };
   issue(0, a0, b0);
@@ -496,12 +501,13 @@ __global__ void __launch_bounds__(512, 1) gemm_bk32(GemmParams p) {
 // Two stages of 64 k (32 KB per operand each, 128 KB in all).  A KC copy
 // instruction moves 8 whole rows of 128 bytes (one cache line each, so no
 // line is fetched twice); an MN copy instruction moves 2 k-rows of 512 bytes.
-// KC slot s of row r holds chunk s ^ (r & 7): the 8 rows one 8-lane group of a
-// fragment read touches cover all 32 banks once.
+// KC slot s of row r holds chunk s ^ ((r >> 1) & 7).  Two rows share a 256-byte
+// bank line (r % 2 picks the half), so the 16 rows one 16-lane group of a
+// fragment read touches cover all 64 banks once.
 constexpr int BK2 = 64;
 constexpr int TILE2 = 256 * BK2 * 2;     // 32 KB per operand per stage
 
-__device__ __forceinline__ int kc2_off(int row, int chunk) { return row * 128 + ((chunk ^ (row & 7)) << 4); }
+__device__ __forceinline__ int kc2_off(int row, int chunk) { return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4); }
 
 template <int WAVES>
 struct Kc2Rows {
@@ -509,10 +515,12 @@ struct Kc2Rows {
   int c8;
 };
 
+// Copy q of wave w moves rows 8 kb + lane/8, kb = w + WAVES q; (row >> 1) & 7 =
+// 4 (w & 1) + lane/16 is the same for every q.
 template <int WAVES>
 __device__ __forceinline__ Kc2Rows<WAVES> kc2_rows(const Operand& op, int x0, int tile_idx, int wave, int lane) {
   Kc2Rows<WAVES> r;
-  r.c8 = 8 * ((lane & 7) ^ ((lane >> 3) & 7));
+  r.c8 = 8 * ((lane & 7) ^ (4 * (wave & 1) + (lane >> 4)));
 #pragma unroll
   for (int q = 0; q < 32 / WAVES; ++q) {
     const int xr = 8 * (wave + WAVES * q) + (lane >> 3);
@@ -690,6 +698,10 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
     wait_vm<0>();
     stage_barrier();
     issue(min(kt + 2, nk - 1) * BK2, xa, xb);
+    // Keep the copies here, right after the barrier: left alone, the scheduler
+    // sinks them to the end of the next stage, next to the wait for them, and
+    // no computation overlaps their latency.
+    __builtin_amdgcn_sched_barrier(0);
     read_frags2<LA, LB, NS>(f0, ya, yb, wm, ncol, 0, lane);   // after the last stage: read, never used
     mfma_frags2<NS>(acc, f1);
     interleave2<LA, LB, NS>();
