@@ -55,6 +55,18 @@ constexpr int GROUP_M = 8;
 
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
+// Direct-to-LDS copy: 16 bytes per lane from g into the wave's 1 KB LDS chunk
+// at lds (lane i lands at byte 16 i).  Inline assembly, so that the compiler's
+// wait-count pass does not see an LDS write in flight: it cannot tell one
+// stage buffer from another and would wait for every copy before the first
+// LDS read of the next stage, exposing the copy latency on every stage.  The
+// kernels wait for their own copies (vmcnt) before the barrier that publishes
+// a stage, and before the stages are reused as epilogue staging space.
+__device__ __forceinline__ void dma16(const uint16_t* g, const uint8_t* lds) {
+  const uint32_t l = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LPTR(const_cast<uint8_t*>(lds))));
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(l) : "memory", "m0");
+}
+
 __device__ __forceinline__ u32x4 pack8(const float* v) {
   u32x4 r;
 #pragma unroll
@@ -130,7 +142,7 @@ __device__ __forceinline__ void copy_kc(uint8_t* lds, const KcRows<WAVES>& rows,
   if constexpr (RAGGED) k = min(k, K - 8);
 #pragma unroll
   for (int q = 0; q < 16 / WAVES; ++q)
-    __builtin_amdgcn_global_load_lds(GPTR(rows.row[q] + k), LPTR(lds + (wave + WAVES * q) * 1024), 16, 0, 0);
+    dma16(rows.row[q] + k, lds + (wave + WAVES * q) * 1024);
 }
 
 template <int WAVES>
@@ -147,8 +159,7 @@ __device__ __forceinline__ void copy_mn(uint8_t* lds, const Operand& op, int x0,
     if (x >= op.rows) x = op.rows - 8;
     const uint32_t o = op.src.row_index(k);
     const uint16_t* base = (o & 0x80000000u) ? op.src.peer : op.src.own;
-    __builtin_amdgcn_global_load_lds(GPTR(base + static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld + x),
-                                     LPTR(lds + kb * 1024), 16, 0, 0);
+    dma16(base + static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld + x, lds + kb * 1024);
   }
 }
 
@@ -489,6 +500,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bk32(GemmParams p) {
   if (rest > 0) step(kt, a0, b0, a3, b3);
   if (rest > 1) step(kt + 1, a1, b1, a0, b0);
   if (rest > 2) step(kt + 2, a2, b2, a1, b1);
+  wait_vm<0>();      // no copy may land in the stages once they are staging space
   __syncthreads();   // every wave is done reading the stages before they become staging space
 
   uint8_t* mine = wave == 0 ? a0 : wave == 1 ? b0 : wave == 2 ? a1 : wave == 3 ? b1 : wave == 4 ? a2
@@ -543,7 +555,7 @@ __device__ __forceinline__ void copy2_kc(uint8_t* lds, const Kc2Rows<WAVES>& row
   const int k = k0 + rows.c8;
 #pragma unroll
   for (int q = 0; q < 32 / WAVES; ++q)
-    __builtin_amdgcn_global_load_lds(GPTR(rows.row[q] + k), LPTR(lds + (wave + WAVES * q) * 1024), 16, 0, 0);
+    dma16(rows.row[q] + k, lds + (wave + WAVES * q) * 1024);
 }
 
 // MN copies.  For an operand whose rows are one plain array (no sequence-
@@ -572,7 +584,7 @@ __device__ __forceinline__ void copy2_mn(uint8_t* lds, const Operand& op, const 
 #pragma unroll
     for (int q = 0; q < 32 / WAVES; ++q) {
       const uint16_t* base = op.src.own + static_cast<int64_t>(k0 + 2 * WAVES * q) * op.src.ld;
-      __builtin_amdgcn_global_load_lds(GPTR(base + rows.off0), LPTR(lds + (wave + WAVES * q) * 1024), 16, 0, 0);
+      dma16(base + rows.off0, lds + (wave + WAVES * q) * 1024);
     }
     return;
   }
@@ -585,8 +597,7 @@ __device__ __forceinline__ void copy2_mn(uint8_t* lds, const Operand& op, const 
     if (x >= op.rows) x = op.rows - 8;
     const uint32_t o = op.src.row_index(k0 + kr);
     const uint16_t* base = (o & 0x80000000u) ? op.src.peer : op.src.own;
-    __builtin_amdgcn_global_load_lds(GPTR(base + static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld + x),
-                                     LPTR(lds + kb * 1024), 16, 0, 0);
+    dma16(base + static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld + x, lds + kb * 1024);
   }
 }
 
@@ -717,7 +728,8 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
     stage(kt, a0, b0, a1, b1);
     stage(kt + 1, a1, b1, a0, b0);
   }
-  __syncthreads();   // every copy has landed and every wave is done reading the stages
+  wait_vm<0>();      // the last (repeated) stage copy has landed
+  __syncthreads();   // every wave is done reading the stages
 
   uint8_t* mine = (WAVES == 8 ? (wave >> 1) : wave) == 0 ? a0
                 : (WAVES == 8 ? (wave >> 1) : wave) == 1 ? b0
