@@ -42,7 +42,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-#define GPTR(p) ((const __attribute__((address_space(1))) void*)(p))
 #define LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
 constexpr float kLog2e = 1.4426950408889634f;
@@ -93,15 +92,28 @@ __device__ __forceinline__ int swz(int row) {
   return D == 128 ? ((((row & 3) ^ b3) << 2) | (b2 << 1) | (row & 1)) : (((b1 ^ b3) << 2) | (b2 << 1) | b1);
 }
 
+// Direct-to-LDS copy of `size` bytes per lane from sbase + voff (uniform base,
+// per-lane byte offset) into the wave's LDS chunk at lds (lane i lands at
+// lds + size * i).  Inline assembly: the compiler's wait-count pass does not
+// see the LDS write in flight, so it does not drain the prefetch before the
+// reads of the other buffer (it cannot tell the buffers apart).  The kernels
+// wait for their own copies (vmcnt) before the barrier that publishes a tile.
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, const uint8_t* lds) {
+  const uint32_t l = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LPTR(const_cast<uint8_t*>(lds))));
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(l) : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(const void* sbase, uint32_t voff, const void* lds) {
+  const uint32_t l = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LPTR(const_cast<void*>(lds))));
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(voff), "s"(sbase), "s"(l) : "memory", "m0");
+}
+
 // Copy rows [0, ROWS) of src (row stride ld, rows >= n_valid clamped to the
 // last valid row) into an LDS tile; the NW waves of the block share the work.
 // A copy instruction moves RPK whole rows (1 KB); lane i lands at byte 16 i of
 // the instruction's LDS chunk.  The wave's copies start at rows that agree
 // modulo 4 * RPK (the waves take every NW-th chunk, NW a multiple of 4), which
-// fixes swz, so each lane's swizzled source column is fixed: a buffer load with
-// the tile base in the (uniform) resource, the row block in the scalar offset
-// and one 32-bit per-lane offset, except on a ragged tail.
-constexpr int kBufferDword3 = 0x00020000;    // raw buffer, 32-bit data format (gfx9 family)
+// fixes swz, so each lane's swizzled source column is fixed: the row block is
+// a uniform base and the lane adds one 32-bit byte offset, except on a ragged tail.
 template <int D, int ROWS, int NW = 4>
 __device__ __forceinline__ void tile_load(uint8_t* lds, const uint16_t* src, int64_t ld, int n_valid, int wave,
                                           int lane) {
@@ -109,8 +121,6 @@ __device__ __forceinline__ void tile_load(uint8_t* lds, const uint16_t* src, int
   constexpr int RPK = 64 / CH;           // rows per 1 KB wave chunk
   constexpr int NKB = ROWS / RPK;
   static_assert(NKB % NW == 0, "every wave issues the same number of copies");
-  const __amdgpu_buffer_rsrc_t rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(src), 0, -1, kBufferDword3);
   const int lrow = lane / CH;
   const int lc = (lane % CH) ^ swz<D>(wave * RPK + lrow);   // the same for every copy of this wave
   const int ldb = static_cast<int>(ld) * 2;                 // row stride in bytes
@@ -119,15 +129,14 @@ __device__ __forceinline__ void tile_load(uint8_t* lds, const uint16_t* src, int
 #pragma unroll
     for (int j = 0; j < NKB / NW; ++j) {
       const int q = wave + j * NW;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LPTR(lds + q * 1024), 16, lane_off, q * RPK * ldb, 0, 0);
+      dma16(src + static_cast<int64_t>(q * RPK) * ld, lane_off, lds + q * 1024);
     }
   } else {                               // ragged tail: rows past n_valid repeat the last valid row
 #pragma unroll
     for (int j = 0; j < NKB / NW; ++j) {
       const int q = wave + j * NW;
       const int r = min(q * RPK + lrow, n_valid - 1);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LPTR(lds + q * 1024), 16, static_cast<uint32_t>(r * ldb + lc * 16),
-                                               0, 0, 0);
+      dma16(src, static_cast<uint32_t>(r * ldb + lc * 16), lds + q * 1024);
     }
   }
 }
@@ -537,9 +546,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int hq = head0 + it / n_qt, qt = it % n_qt;
     if (lane < 16) {    // waves 0-3 copy the lse, waves 4-7 delta, of queries 16 grp .. 16 grp + 15
       const int q = min(qt * QT + grp * 16 + lane, p.n_q - 1);
-      const int64_t idx = (static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + q;
-      __builtin_amdgcn_global_load_lds(GPTR((role == 0 ? p.lse : p.delta) + idx), LPTR(&st[role][grp * 16]), 4, 0,
-                                       0);
+      const float* row = (role == 0 ? p.lse : p.delta) + (static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q;
+      dma4(row, static_cast<uint32_t>(q) * 4u, &st[role][grp * 16]);
     }
     const int64_t off = bi * p.q_bstride + static_cast<int64_t>(qt * QT) * p.q_ld + hq * D;
     tile_load<D, QT, 8>(qt_l, p.q + off, p.q_ld, p.n_q - qt * QT, wave, lane);
