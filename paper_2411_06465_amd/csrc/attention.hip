@@ -98,12 +98,16 @@ __device__ __forceinline__ int swz(int row) {
 // see the LDS write in flight, so it does not drain the prefetch before the
 // reads of the other buffer (it cannot tell the buffers apart).  The kernels
 // wait for their own copies (vmcnt) before the barrier that publishes a tile.
+// The LDS address is uniform by construction; readfirstlane states it for the
+// compiler, which otherwise may keep it in a vector register.
 __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, const uint8_t* lds) {
-  const uint32_t l = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LPTR(const_cast<uint8_t*>(lds))));
+  const uint32_t l = __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LPTR(const_cast<uint8_t*>(lds)))));
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(l) : "memory", "m0");
 }
 __device__ __forceinline__ void dma4(const void* sbase, uint32_t voff, const void* lds) {
-  const uint32_t l = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LPTR(const_cast<void*>(lds))));
+  const uint32_t l = __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LPTR(const_cast<void*>(lds)))));
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(voff), "s"(sbase), "s"(l) : "memory", "m0");
 }
 

@@ -63,7 +63,8 @@ __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(ui
 // kernels wait for their own copies (vmcnt) before the barrier that publishes
 // a stage, and before the stages are reused as epilogue staging space.
 __device__ __forceinline__ void dma16(const uint16_t* g, const uint8_t* lds) {
-  const uint32_t l = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LPTR(const_cast<uint8_t*>(lds))));
+  const uint32_t l = __builtin_amdgcn_readfirstlane(   // uniform by construction; stated for the compiler
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LPTR(const_cast<uint8_t*>(lds)))));
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(l) : "memory", "m0");
 }
 
@@ -616,13 +617,17 @@ __device__ __forceinline__ bf16x8 frag2(const uint8_t* lds, int x0, int kk, int 
   }
 }
 
+// Fragments are read in the order the products consume them (A0, B0 .. B(NS-1),
+// A1, A2, A3), so the first products of the next sub-step wait on the
+// earliest reads.
 template <Layout LA, Layout LB, int NS>
 __device__ __forceinline__ void read_frags2(Frags2<NS>& f, const uint8_t* la, const uint8_t* lb, int wm,
                                             const int* ncol, int kk, int lane) {
-#pragma unroll
-  for (int ms = 0; ms < 4; ++ms) f.a[ms] = frag2<LA>(la, wm * 128 + ms * 32, kk, lane);
+  f.a[0] = frag2<LA>(la, wm * 128, kk, lane);
 #pragma unroll
   for (int ns = 0; ns < NS; ++ns) f.b[ns] = frag2<LB>(lb, ncol[ns], kk, lane);
+#pragma unroll
+  for (int ms = 1; ms < 4; ++ms) f.a[ms] = frag2<LA>(la, wm * 128 + ms * 32, kk, lane);
 }
 
 template <int NS>
@@ -635,8 +640,7 @@ __device__ __forceinline__ void mfma_frags2(f32x16 (&acc)[4][NS], const Frags2<N
 }
 
 // Spread DS reads over the MFMAs of a sub-step: 8 slots of (DS share, M MFMAs).
-// Only when both operands are K-contiguous: with a transposed operand (two
-// transposing reads per fragment) the compiler's own order measured faster.
+// A K-contiguous fragment is one LDS read, a transposed one two.
 template <int DS, int M, int I = 0>
 __device__ __forceinline__ void interleave2_slots() {
   if constexpr (I < 8) {
@@ -648,7 +652,8 @@ __device__ __forceinline__ void interleave2_slots() {
 }
 template <Layout LA, Layout LB, int NS>
 __device__ __forceinline__ void interleave2() {
-  if constexpr (LA == Layout::KC && LB == Layout::KC) interleave2_slots<4 + NS, NS / 2>();
+  constexpr int DS = 4 * (LA == Layout::KC ? 1 : 2) + NS * (LB == Layout::KC ? 1 : 2);
+  interleave2_slots<DS, NS / 2>();
 }
 
 template <Layout LA, Layout LB, EpiKind KIND, int PAIR, int WAVES>
