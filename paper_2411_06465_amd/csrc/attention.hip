@@ -74,6 +74,15 @@ __device__ __forceinline__ void ring_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Make the compiler wait for a value loaded from global memory here, before
+// the tile loop: otherwise it places the wait at the value's first use inside
+// the loop, on every iteration, where the hardware counter also holds the
+// next tile's copies (issued as inline assembly) -- and the wait drains them.
+template <class T>
+__device__ __forceinline__ void settle(const T& v) {
+  asm volatile("" ::"v"(v));
+}
+
 // ------------------------------------------------------------------ LDS tiles
 // Row-major [rows][D] bf16 tile; 16-byte chunk c of row r sits at chunk c ^ swz(r).
 // The LDS serves 256 bytes (64 banks) per cycle.  Two read patterns must be
@@ -319,6 +328,8 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))
     const uint16_t* qb = p.q + bi * p.q_bstride + static_cast<int64_t>(q_ok ? my_q : 0) * p.q_ld + hq * D;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qb + (2 * kk + (lane >> 5)) * 8);
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) settle(qf[kk]);
   }
   const float c = p.scale * kLog2e;
   float m_run = -INFINITY, l_run = 0.f;
@@ -530,6 +541,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk)
       kv[kk] = *reinterpret_cast<const bf16x8*>(src + off + (2 * kk + (lane >> 5)) * 8);
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) settle(kv[kk]);
   }
   f32x16 acc[D / 32];                    // role 0: dV^T, role 1: dK^T (d rows, the lane's key)
 #pragma unroll
@@ -804,6 +817,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int64_t sidx = (static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + (q_ok ? my_q : 0);
   const float my_lse = p.lse[sidx] * kLog2e;
   const float my_delta = p.delta[sidx];
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) {
+    settle(qf[kk]);
+    settle(dof[kk]);
+  }
+  settle(my_lse);
+  settle(my_delta);
   const float c = p.scale * kLog2e;
   f32x16 dq[D / 32];
 #pragma unroll
