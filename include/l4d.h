@@ -251,6 +251,9 @@ int lm_head_xent(int64_t n_tokens, int64_t hidden, int64_t vocab_shard, int64_t 
 
 /* on != 0: record a start/stop event pair around each kernel launch. */
 int l4d_profile_enable(int on);
+/* Restrict the timing to the launches labelled `name` (NULL or "": all
+ * launches).  Each timed launch adds its event pair to the stream. */
+int l4d_profile_only(const char* name);
 /* Synchronize the recorded events and return, for the kernel `name`, the
  * number of timed launches and the summed duration in milliseconds.  With
  * name == NULL, the totals over all kernels. */

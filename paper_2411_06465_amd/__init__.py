@@ -88,6 +88,7 @@ def lib():
                                  P, P, P, P], C.c_int),
             "lm_head_xent": ([i64, i64, i64, i64, P, P, P, P, P, f32, P, P, P, P, P], C.c_int),
             "l4d_profile_enable": ([C.c_int], C.c_int),
+            "l4d_profile_only": ([C.c_char_p], C.c_int),
             "l4d_profile_read": ([C.c_char_p, C.POINTER(i64), C.POINTER(C.c_double)], C.c_int),
             "l4d_profile_dump": ([C.c_char_p, u64, C.POINTER(u64)], C.c_int),
             "l4d_profile_reset": ([], C.c_int),
@@ -247,6 +248,10 @@ def lm_head_xent(hidden, w_lm, targets, loss, d_hidden, d_w_lm, arena, vocab_sta
 
 def l4d_profile_enable(on=True):
     _check(lib().l4d_profile_enable(1 if on else 0))
+
+
+def l4d_profile_only(name=None):
+    _check(lib().l4d_profile_only(name.encode() if name else None))
 
 
 def l4d_profile_reset():

@@ -50,6 +50,7 @@ struct Pending {
 };
 std::mutex g_prof_mu;
 bool g_prof_on = false;
+std::string g_prof_only;            // non-empty: time only the launches with this label
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_event_pool;
 std::map<std::string, std::pair<int64_t, double>> g_totals;
@@ -85,7 +86,7 @@ int drain_pending() {
 template <class F>
 int launch(const char* name, hipStream_t s, F&& fn) {
   hipEvent_t a = nullptr, b = nullptr;
-  if (g_prof_on) {
+  if (g_prof_on && (g_prof_only.empty() || g_prof_only == name)) {
     std::lock_guard<std::mutex> lk(g_prof_mu);
     a = take_event();
     b = take_event();
@@ -105,6 +106,12 @@ int launch(const char* name, hipStream_t s, F&& fn) {
 extern "C" int l4d_profile_enable(int on) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   g_prof_on = on != 0;
+  return L4D_OK;
+}
+
+extern "C" int l4d_profile_only(const char* name) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_only = name ? name : "";
   return L4D_OK;
 }
 
