@@ -13,7 +13,9 @@
 //    fragments of the next 16-k sub-step are read from LDS under the MFMAs of
 //    the current one, and the barrier that publishes stage kt+1 sits before
 //    the last sub-step of stage kt, right after which the freed buffers take
-//    stage kt+2.  8 waves (two per SIMD, 128x64 each) or 4 (128x128 each).
+//    stage kt+2 (the A half there, the B half one sub-step later, so the
+//    copies do not all reach the texture path at once).  8 waves (two per
+//    SIMD, 128x64 each) or 4 (128x128 each).
 //  * gemm_bk32 (any K that is a multiple of 8): 8 waves, four stages of 32 k,
 //    16 rows x 64 bytes per copy instruction, the stage past K zeroed in
 //    registers.
@@ -30,7 +32,9 @@
 // A wave's 32-column blocks come in pairs PAIR columns apart, so the columns
 // n and n + PAIR land in the same lane and register: a RoPE pair (i, i + d_h/2)
 // or a gate/up pair of the fused FFN weight.  The epilogue stages rows through
-// LDS and hands 8-column vectors to the fused operation.
+// LDS and hands 8-column vectors to the fused operation, with that operation's
+// global inputs loaded for a whole pass first.  The fp32 accumulate (dW) needs
+// no staging: the accumulators start from the C tile and are stored back.
 #include <stdlib.h>
 
 #include "kernels.h"
@@ -186,11 +190,81 @@ __device__ __forceinline__ bf16x8 frag(const uint8_t* lds, int x0, int kk, int l
 
 // -------------------------------------------------------------- epilogues
 
-__device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
+// silu(g) = g * sigmoid(g); the reciprocal is the hardware one (1 ulp), far
+// below the bf16 rounding of every value it feeds.
+__device__ __forceinline__ float sigmoid_f(float g) { return __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
+
+// Global inputs of one epilogue call (8 columns at `col` and the 8 PAIR
+// further), loaded for a whole pass of the staged epilogue before the tile is
+// staged, so that their latencies overlap instead of adding up.
+template <EpiKind KIND>
+struct EpiIn {};
+template <>
+struct EpiIn<EpiKind::ResidualSP> {
+  u32x4 r[2], q[2];       // residual, receipt: low and high half
+};
+template <>
+struct EpiIn<EpiKind::SwiGLUBwd> {
+  u32x4 g[2], u[2], a[2];
+};
+template <>
+struct EpiIn<EpiKind::QkvRope> {
+  float4 cs[4];           // (cos, sin) of the 8 columns
+};
+
+// Output row of logical row m for ResidualSP: own rows map into own_out,
+// the others into the send buffer.
+__device__ __forceinline__ int64_t resid_row(const EpiParams& e, int64_t m, bool& own) {
+  own = true;
+  if (e.t == 1) return m;
+  const int64_t bi = m / e.s_c;
+  const int32_t i = static_cast<int32_t>(m - bi * e.s_c);
+  const int32_t lo_row = e.r * e.s_sp;
+  own = i >= lo_row && i < lo_row + e.s_sp;
+  return own ? bi * e.s_sp + (i - lo_row) : bi * static_cast<int64_t>(e.t - 1) * e.s_sp + (i < lo_row ? i : i - e.s_sp);
+}
+
+template <EpiKind KIND, int PAIR>
+__device__ __forceinline__ void epi_load(const GemmParams& p, int64_t m, int tn, int col, EpiIn<KIND>& in) {
+  const EpiParams& e = p.epi;
+  if (m >= p.M) return;
+  const int n_lo = tn * BN + col;
+  if constexpr (KIND == EpiKind::ResidualSP) {
+    bool own;
+    const int64_t orow = resid_row(e, m, own);
+    if (!own) return;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int n = n_lo + h * PAIR;
+      if (n >= p.N) continue;
+      const int64_t off = orow * e.ldc + n;
+      if (e.resid) in.r[h] = *reinterpret_cast<const u32x4*>(e.resid + off);
+      if (e.receipt) in.q[h] = *reinterpret_cast<const u32x4*>(e.receipt + off);
+    }
+  } else if constexpr (KIND == EpiKind::SwiGLUBwd) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int n = n_lo + h * PAIR;
+      if (n >= p.N) continue;
+      const int64_t off = m * e.f + n;
+      in.g[h] = *reinterpret_cast<const u32x4*>(e.g_in + off);
+      in.u[h] = *reinterpret_cast<const u32x4*>(e.u_in + off);
+      in.a[h] = *reinterpret_cast<const u32x4*>(e.act_in + off);
+    }
+  } else if constexpr (KIND == EpiKind::QkvRope) {
+    if (n_lo >= p.N || n_lo >= e.nq + e.nk) return;     // V columns are not rotated
+    const int n = n_lo < e.nq ? n_lo : n_lo - e.nq;
+    const int32_t i = static_cast<int32_t>(m % e.s_c);
+    const float4* tab = reinterpret_cast<const float4*>(e.rope + static_cast<int64_t>(i) * (e.d_h / 2) + (n % e.d_h));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) in.cs[j] = tab[j];
+  }
+}
 
 // lo: 8 columns starting at tile column `col`; hi: the 8 columns PAIR further.
 template <EpiKind KIND, int PAIR>
-__device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn, int col, float* lo, float* hi) {
+__device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn, int col, float* lo, float* hi,
+                                         const EpiIn<KIND>& in) {
   const EpiParams& e = p.epi;
   if (m >= p.M) return;
   const int n_lo = tn * BN + col;
@@ -201,83 +275,63 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn,
       if (n_lo + PAIR < p.N) *reinterpret_cast<u32x4*>(c + n_lo + PAIR) = pack8(hi);
       break;
     }
-    case EpiKind::AccF32: {
-      float* c = static_cast<float*>(e.c) + m * e.ldc;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int n = n_lo + h * PAIR;
-        const float* src = h ? hi : lo;
-        if (n < p.N) {
-          float4* d = reinterpret_cast<float4*>(c + n);
-          float4 a = d[0], b = d[1];
-          a.x += src[0]; a.y += src[1]; a.z += src[2]; a.w += src[3];
-          b.x += src[4]; b.y += src[5]; b.z += src[6]; b.w += src[7];
-          d[0] = a;
-          d[1] = b;
-        }
-      }
+    case EpiKind::AccF32:     // handled in registers (acc_load_f32 / acc_store_f32)
       break;
-    }
     case EpiKind::QkvRope: {
-      // n_lo lies in the first half of a head, n_lo + PAIR (PAIR = d_h/2) in the second.
-      if (n_lo >= p.N) break;
-      uint16_t* dst;
-      int64_t ld;
-      int n;
-      bool rot = true;
-      if (n_lo < e.nq) { dst = e.q; ld = e.nq; n = n_lo; }
-      else if (n_lo < e.nq + e.nk) { dst = e.k; ld = e.nk; n = n_lo - e.nq; }
-      else { dst = e.v; ld = e.nk; n = n_lo - e.nq - e.nk; rot = false; }
-      if (rot) {
-        const int32_t i = static_cast<int32_t>(m % e.s_c);
-        const float2* tab = e.rope + static_cast<int64_t>(i) * (e.d_h / 2) + (n % e.d_h);
-        float a[8], b[8];
+      if constexpr (KIND == EpiKind::QkvRope) {
+        // n_lo lies in the first half of a head, n_lo + PAIR (PAIR = d_h/2) in the second.
+        if (n_lo >= p.N) break;
+        uint16_t* dst;
+        int64_t ld;
+        int n;
+        bool rot = true;
+        if (n_lo < e.nq) { dst = e.q; ld = e.nq; n = n_lo; }
+        else if (n_lo < e.nq + e.nk) { dst = e.k; ld = e.nk; n = n_lo - e.nq; }
+        else { dst = e.v; ld = e.nk; n = n_lo - e.nq - e.nk; rot = false; }
+        if (rot) {
+          float a[8], b[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float2 cs = tab[j];
-          a[j] = lo[j] * cs.x - hi[j] * cs.y;
-          b[j] = hi[j] * cs.x + lo[j] * cs.y;
+          for (int j = 0; j < 8; ++j) {
+            const float c = j & 1 ? in.cs[j >> 1].z : in.cs[j >> 1].x;
+            const float sn = j & 1 ? in.cs[j >> 1].w : in.cs[j >> 1].y;
+            a[j] = lo[j] * c - hi[j] * sn;
+            b[j] = hi[j] * c + lo[j] * sn;
+          }
+          *reinterpret_cast<u32x4*>(dst + m * ld + n) = pack8(a);
+          *reinterpret_cast<u32x4*>(dst + m * ld + n + PAIR) = pack8(b);
+        } else {
+          *reinterpret_cast<u32x4*>(dst + m * ld + n) = pack8(lo);
+          *reinterpret_cast<u32x4*>(dst + m * ld + n + PAIR) = pack8(hi);
         }
-        *reinterpret_cast<u32x4*>(dst + m * ld + n) = pack8(a);
-        *reinterpret_cast<u32x4*>(dst + m * ld + n + PAIR) = pack8(b);
-      } else {
-        *reinterpret_cast<u32x4*>(dst + m * ld + n) = pack8(lo);
-        *reinterpret_cast<u32x4*>(dst + m * ld + n + PAIR) = pack8(hi);
       }
       break;
     }
     case EpiKind::ResidualSP: {
-      int64_t orow = m;
-      bool own = true;
-      if (e.t > 1) {
-        const int64_t bi = m / e.s_c;
-        const int32_t i = static_cast<int32_t>(m - bi * e.s_c);
-        const int32_t lo_row = e.r * e.s_sp;
-        own = i >= lo_row && i < lo_row + e.s_sp;
-        orow = own ? bi * e.s_sp + (i - lo_row)
-                   : bi * static_cast<int64_t>(e.t - 1) * e.s_sp + (i < lo_row ? i : i - e.s_sp);
-      }
+      if constexpr (KIND == EpiKind::ResidualSP) {
+        bool own;
+        const int64_t orow = resid_row(e, m, own);
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int n = n_lo + h * PAIR;
-        if (n >= p.N) continue;
-        float* src = h ? hi : lo;
-        const int64_t off = orow * e.ldc + n;
-        if (own) {
-          float r[8];
-          if (e.resid) {
-            unpack8(*reinterpret_cast<const u32x4*>(e.resid + off), r);
+        for (int h = 0; h < 2; ++h) {
+          const int n = n_lo + h * PAIR;
+          if (n >= p.N) continue;
+          float* src = h ? hi : lo;
+          const int64_t off = orow * e.ldc + n;
+          if (own) {
+            float r[8];
+            if (e.resid) {
+              unpack8(in.r[h], r);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) src[j] += r[j];
+              for (int j = 0; j < 8; ++j) src[j] += r[j];
+            }
+            if (e.receipt) {
+              unpack8(in.q[h], r);
+#pragma unroll
+              for (int j = 0; j < 8; ++j) src[j] += r[j];
+            }
+            *reinterpret_cast<u32x4*>(e.own_out + off) = pack8(src);
+          } else {
+            *reinterpret_cast<u32x4*>(e.send + off) = pack8(src);
           }
-          if (e.receipt) {
-            unpack8(*reinterpret_cast<const u32x4*>(e.receipt + off), r);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) src[j] += r[j];
-          }
-          *reinterpret_cast<u32x4*>(e.own_out + off) = pack8(src);
-        } else {
-          *reinterpret_cast<u32x4*>(e.send + off) = pack8(src);
         }
       }
       break;
@@ -291,7 +345,7 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn,
       unpack8(pack8(hi), u);
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
-        a[q] = silu_f(g[q]);
+        a[q] = g[q] * sigmoid_f(g[q]);
         pr[q] = a[q] * u[q];
       }
       *reinterpret_cast<u32x4*>(e.g_out + off) = pack8(g);
@@ -301,25 +355,27 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn,
       break;
     }
     case EpiKind::SwiGLUBwd: {
+      if constexpr (KIND == EpiKind::SwiGLUBwd) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int n = n_lo + h * PAIR;
-        if (n >= p.N) continue;
-        const float* dp = h ? hi : lo;
-        const int64_t off = m * e.f + n;
-        float g[8], u[8], a[8], dg[8], du[8];
-        unpack8(*reinterpret_cast<const u32x4*>(e.g_in + off), g);
-        unpack8(*reinterpret_cast<const u32x4*>(e.u_in + off), u);
-        unpack8(*reinterpret_cast<const u32x4*>(e.act_in + off), a);
+        for (int h = 0; h < 2; ++h) {
+          const int n = n_lo + h * PAIR;
+          if (n >= p.N) continue;
+          const float* dp = h ? hi : lo;
+          const int64_t off = m * e.f + n;
+          float g[8], u[8], a[8], dg[8], du[8];
+          unpack8(in.g[h], g);
+          unpack8(in.u[h], u);
+          unpack8(in.a[h], a);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const float s = 1.0f / (1.0f + __expf(-g[q]));
-          dg[q] = dp[q] * u[q] * (s * (1.0f + g[q] * (1.0f - s)));
-          du[q] = dp[q] * a[q];
+          for (int q = 0; q < 8; ++q) {
+            const float s = sigmoid_f(g[q]);
+            dg[q] = dp[q] * u[q] * (s * (1.0f + g[q] * (1.0f - s)));
+            du[q] = dp[q] * a[q];
+          }
+          uint16_t* out = e.dgu + m * (2 * static_cast<int64_t>(e.f));
+          *reinterpret_cast<u32x4*>(out + n) = pack8(dg);
+          *reinterpret_cast<u32x4*>(out + e.f + n) = pack8(du);
         }
-        uint16_t* out = e.dgu + m * (2 * static_cast<int64_t>(e.f));
-        *reinterpret_cast<u32x4*>(out + n) = pack8(dg);
-        *reinterpret_cast<u32x4*>(out + e.f + n) = pack8(du);
       }
       break;
     }
@@ -365,13 +421,23 @@ __device__ __forceinline__ void wait_vm() {
 // own 16 KB of LDS (column halves swapped on rows with bit 2 set, so the two
 // half-waves write different banks) and hands out 8-column vectors of its low
 // blocks with their PAIR partners.  Accumulator register i of a lane: row
-// 8(i/4) + 4(lane/32) + i%4, column lane%32 of its 32x32 tile.
+// 8(i/4) + 4(lane/32) + i%4, column lane%32 of its 32x32 tile.  The global
+// inputs of a pass are loaded before its rows are staged.
 template <EpiKind KIND, int PAIR, int NS>
 __device__ __forceinline__ void store_tile(const GemmParams& p, f32x16 (&acc)[4][NS], float* st, int64_t row0,
                                            int tn, const int* ncol, int lane) {
   constexpr int C = NS * 32, R = 4096 / C, PASSES = 128 / R, MS_PER = R / 32;
+  constexpr int VEC = R * (NS / 2) * 4;  // 8-column vectors of the low blocks per pass
+  constexpr int ITERS = VEC / 64;
 #pragma unroll
   for (int pass = 0; pass < PASSES; ++pass) {
+    EpiIn<KIND> in[ITERS];
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+      const int idx = it * 64 + lane;
+      const int rr = idx / ((NS / 2) * 4), v = idx % ((NS / 2) * 4);
+      epi_load<KIND, PAIR>(p, row0 + pass * R + rr, tn, ncol[v >> 2] + (v & 3) * 8, in[it]);
+    }
 #pragma unroll
     for (int mm = 0; mm < MS_PER; ++mm)
 #pragma unroll
@@ -383,9 +449,8 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, f32x16 (&acc)[4]
           st[r * C + cc] = acc[pass * MS_PER + mm][ns][i];
         }
     __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-    constexpr int VEC = R * (NS / 2) * 4;  // 8-column vectors of the low blocks per pass
-#pragma unroll 1
-    for (int it = 0; it < VEC / 64; ++it) {
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
       const int idx = it * 64 + lane;
       const int rr = idx / ((NS / 2) * 4), v = idx % ((NS / 2) * 4);
       const int j = v >> 2, c8 = (v & 3) * 8;
@@ -395,10 +460,77 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, f32x16 (&acc)[4]
       const float4 l0 = lo4[0], l1 = lo4[1], h0 = hi4[0], h1 = hi4[1];
       float lo[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
       float hi[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
-      epilogue<KIND, PAIR>(p, row0 + pass * R + rr, tn, ncol[j] + c8, lo, hi);
+      epilogue<KIND, PAIR>(p, row0 + pass * R + rr, tn, ncol[j] + c8, lo, hi, in[it]);
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);
   }
+}
+
+// AccF32 (C += A B^T in fp32) works on the accumulators directly: the tile of C
+// is loaded into them before the first product (its latency overlaps the first
+// stage's copies) and stored from them at the end.  In the accumulator layout
+// the 32 lanes of a half-wave cover 32 consecutive columns (128 bytes) of one
+// row, so both are whole-line accesses without staging.
+template <int NS>
+__device__ __forceinline__ void acc_load_f32(f32x16 (&acc)[4][NS], const GemmParams& p, int64_t row0, int tn,
+                                             const int* ncol, int lane) {
+  const int64_t ldc = p.epi.ldc;
+  const int rl = 4 * (lane >> 5);
+  int32_t off[NS];            // lane's element offset from its row block's first row
+#pragma unroll
+  for (int ns = 0; ns < NS; ++ns) off[ns] = static_cast<int32_t>(rl * ldc) + tn * BN + ncol[ns] + (lane & 31);
+  const bool full = row0 + 128 <= p.M && (tn + 1) * BN <= p.N;   // uniform
+#pragma unroll
+  for (int ms = 0; ms < 4; ++ms)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = ms * 32 + 8 * (i >> 2) + (i & 3);
+      const float* row = static_cast<const float*>(p.epi.c) + (row0 + r) * ldc;   // uniform
+#pragma unroll
+      for (int ns = 0; ns < NS; ++ns) {
+        if (full) {
+          acc[ms][ns][i] = row[off[ns]];
+        } else {
+          const int n = tn * BN + ncol[ns] + (lane & 31);
+          acc[ms][ns][i] = (row0 + r + rl < p.M && n < p.N) ? row[off[ns]] : 0.0f;
+        }
+      }
+    }
+}
+
+template <int NS>
+__device__ __forceinline__ void acc_store_f32(const f32x16 (&acc)[4][NS], const GemmParams& p, int64_t row0, int tn,
+                                              const int* ncol, int lane) {
+  const int64_t ldc = p.epi.ldc;
+  const int rl = 4 * (lane >> 5);
+  int32_t off[NS];
+#pragma unroll
+  for (int ns = 0; ns < NS; ++ns) off[ns] = static_cast<int32_t>(rl * ldc) + tn * BN + ncol[ns] + (lane & 31);
+  const bool full = row0 + 128 <= p.M && (tn + 1) * BN <= p.N;
+#pragma unroll
+  for (int ms = 0; ms < 4; ++ms)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = ms * 32 + 8 * (i >> 2) + (i & 3);
+      float* row = static_cast<float*>(p.epi.c) + (row0 + r) * ldc;
+#pragma unroll
+      for (int ns = 0; ns < NS; ++ns) {
+        const int n = tn * BN + ncol[ns] + (lane & 31);
+        if (full || (row0 + r + rl < p.M && n < p.N)) row[off[ns]] = acc[ms][ns][i];
+      }
+    }
+}
+
+// Ends the accumulators' pending loads here: an asm that reads and redefines
+// them makes the compiler wait for the loads before it, once, instead of at
+// their first use inside the main loop on every iteration (where the counter
+// also holds the copies of the next stages).
+template <int NS>
+__device__ __forceinline__ void settle_acc(f32x16 (&acc)[4][NS]) {
+#pragma unroll
+  for (int ms = 0; ms < 4; ++ms)
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns) asm volatile("" : "+v"(acc[ms][ns]));
 }
 
 struct TileCoord {
@@ -431,10 +563,14 @@ __global__ void __launch_bounds__(512, 1) gemm_bk32(GemmParams p) {
   ncol[1] = ncol[0] + PAIR;
 
   f32x16 acc[4][NS];
+  if constexpr (KIND == EpiKind::AccF32) {
+    acc_load_f32<NS>(acc, p, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
+  } else {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
+      for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
+  }
 
   KcRows<WAVES> ra{}, rb{};
   if constexpr (LA == Layout::KC) ra = kc_rows<WAVES>(p.A, m0, tm, wave, lane);
@@ -486,6 +622,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bk32(GemmParams p) {
     compute(kt * BK, la, lb);
   };
   issue(0, a0, b0);
+  if constexpr (KIND == EpiKind::AccF32) settle_acc<NS>(acc);   // the C tile (and stage 0) have landed
   if (nk > 1) issue(BK, a1, b1);
   if (nk > 2) issue(2 * BK, a2, b2);
   // Whole groups of 4 steps without early exits (an exit between the unrolled
@@ -501,13 +638,16 @@ __global__ void __launch_bounds__(512, 1) gemm_bk32(GemmParams p) {
   if (rest > 0) step(kt, a0, b0, a3, b3);
   if (rest > 1) step(kt + 1, a1, b1, a0, b0);
   if (rest > 2) step(kt + 2, a2, b2, a1, b1);
-  wait_vm<0>();      // no copy may land in the stages once they are staging space
-  __syncthreads();   // every wave is done reading the stages before they become staging space
-
-  uint8_t* mine = wave == 0 ? a0 : wave == 1 ? b0 : wave == 2 ? a1 : wave == 3 ? b1 : wave == 4 ? a2
-                : wave == 5 ? b2 : wave == 6 ? a3 : b3;
-  store_tile<KIND, PAIR, NS>(p, acc, reinterpret_cast<float*>(mine), static_cast<int64_t>(m0) + wm * 128, tn,
-                             ncol, lane);
+  wait_vm<0>();      // no copy may land in the stages once they are staging space (or after the end)
+  if constexpr (KIND == EpiKind::AccF32) {
+    acc_store_f32<NS>(acc, p, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
+  } else {
+    __syncthreads();   // every wave is done reading the stages before they become staging space
+    uint8_t* mine = wave == 0 ? a0 : wave == 1 ? b0 : wave == 2 ? a1 : wave == 3 ? b1 : wave == 4 ? a2
+                  : wave == 5 ? b2 : wave == 6 ? a3 : b3;
+    store_tile<KIND, PAIR, NS>(p, acc, reinterpret_cast<float*>(mine), static_cast<int64_t>(m0) + wm * 128, tn,
+                               ncol, lane);
+  }
 }
 
 // ---------------------------------------------------------- BK = 64 variant
@@ -675,10 +815,14 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   }
 
   f32x16 acc[4][NS];
+  if constexpr (KIND == EpiKind::AccF32) {
+    acc_load_f32<NS>(acc, p, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
+  } else {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
+      for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
+  }
 
   Kc2Rows<WAVES> ra{}, rb{};
   Mn2Rows ma{}, mb{};
@@ -686,9 +830,11 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   else ma = mn2_rows<WAVES>(p.A, m0, wave, lane);
   if constexpr (LB == Layout::KC) rb = kc2_rows<WAVES>(p.B, n0, tn, wave, lane);
   else mb = mn2_rows<WAVES>(p.B, n0, wave, lane);
-  auto issue = [&](int k0, uint8_t* la, uint8_t* lb) {
+  auto issue_a = [&](int k0, uint8_t* la) {
     if constexpr (LA == Layout::KC) copy2_kc<WAVES>(la, ra, k0, wave);
     else copy2_mn<WAVES>(la, p.A, ma, m0, k0, wave, lane);
+  };
+  auto issue_b = [&](int k0, uint8_t* lb) {
     if constexpr (LB == Layout::KC) copy2_kc<WAVES>(lb, rb, k0, wave);
     else copy2_mn<WAVES>(lb, p.B, mb, n0, k0, wave, lane);
   };
@@ -699,9 +845,16 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   // Stage kt (buffers X, next stage in Y): sub-steps kk = 0..3 each read the
   // fragments of the next sub-step under their own MFMAs.  Before the last
   // sub-step every wave has read all of X: wait for stage kt+1, publish it
-  // with the barrier, refill X with stage kt+2 and read the first fragments
-  // of Y under the last MFMAs.
-  auto stage = [&](int kt, uint8_t* xa, uint8_t* xb, const uint8_t* ya, const uint8_t* yb) {
+  // with the barrier, refill X's A half with stage kt+2 and read the first
+  // fragments of Y under the last MFMAs.  The B half of stage kt+2 follows at
+  // the start of stage kt+1: all 8 waves issuing a whole stage of copies at
+  // the barrier at once fill the texture path's queue, and every wave stalls
+  // at issue with its products waiting behind.
+  auto stage = [&](int kt, uint8_t* xa, uint8_t* xb, const uint8_t* ya, uint8_t* yb) {
+    if (kt > 0) {
+      issue_b(min(kt + 1, nk - 1) * BK2, yb);   // stage kt+1's B half (Y's B buffer was freed at kt-1's barrier)
+      __builtin_amdgcn_sched_barrier(0);
+    }
     read_frags2<LA, LB, NS>(f1, xa, xb, wm, ncol, 1, lane);
     mfma_frags2<NS>(acc, f0);
     interleave2<LA, LB, NS>();
@@ -713,7 +866,7 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
     interleave2<LA, LB, NS>();
     wait_vm<0>();
     stage_barrier();
-    issue(min(kt + 2, nk - 1) * BK2, xa, xb);
+    issue_a(min(kt + 2, nk - 1) * BK2, xa);
     // Keep the copies here, right after the barrier: left alone, the scheduler
     // sinks them to the end of the next stage, next to the wait for them, and
     // no computation overlaps their latency.
@@ -723,8 +876,11 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
     interleave2<LA, LB, NS>();
   };
 
-  issue(0, a0, b0);
-  issue(BK2, a1, b1);
+  issue_a(0, a0);
+  issue_b(0, b0);
+  if constexpr (KIND == EpiKind::AccF32) settle_acc<NS>(acc);   // the C tile (and stage 0) have landed
+  issue_a(BK2, a1);
+  issue_b(BK2, b1);
   if constexpr (PER == 8) wait_vm<16>();
   else wait_vm<8>();
   stage_barrier();
@@ -734,14 +890,17 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
     stage(kt + 1, a1, b1, a0, b0);
   }
   wait_vm<0>();      // the last (repeated) stage copy has landed
-  __syncthreads();   // every wave is done reading the stages
-
-  uint8_t* mine = (WAVES == 8 ? (wave >> 1) : wave) == 0 ? a0
-                : (WAVES == 8 ? (wave >> 1) : wave) == 1 ? b0
-                : (WAVES == 8 ? (wave >> 1) : wave) == 2 ? a1 : b1;
-  if constexpr (WAVES == 8) mine += (wave & 1) * 16384;
-  store_tile<KIND, PAIR, NS>(p, acc, reinterpret_cast<float*>(mine), static_cast<int64_t>(m0) + wm * 128, tn,
-                             ncol, lane);
+  if constexpr (KIND == EpiKind::AccF32) {
+    acc_store_f32<NS>(acc, p, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
+  } else {
+    __syncthreads();   // every wave is done reading the stages
+    uint8_t* mine = (WAVES == 8 ? (wave >> 1) : wave) == 0 ? a0
+                  : (WAVES == 8 ? (wave >> 1) : wave) == 1 ? b0
+                  : (WAVES == 8 ? (wave >> 1) : wave) == 2 ? a1 : b1;
+    if constexpr (WAVES == 8) mine += (wave & 1) * 16384;
+    store_tile<KIND, PAIR, NS>(p, acc, reinterpret_cast<float*>(mine), static_cast<int64_t>(m0) + wm * 128, tn,
+                               ncol, lane);
+  }
 }
 
 // Kernel choice: K a multiple of 128 takes the 8-wave BK = 64 kernel (the
