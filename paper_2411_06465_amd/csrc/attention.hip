@@ -491,7 +491,12 @@ __device__ __forceinline__ void accum_t(const uint8_t* lds, const bf16x8 (&x)[NG
 }
 
 // ------------------------------------------------------------------ backward: dK, dV
-// grid: (key blocks of 128 over all segments, k_t * n_split, b); 8 waves.
+// Flat grid over (key block of 128 over all segments, kv head, split, b), key
+// block slowest: the earliest key blocks see the most query tiles, so they are
+// dispatched first (longest job first keeps the last CUs from running one long
+// block alone), and with the heads varying fastest every block of a head lands
+// on the same XCD (dispatch deals block ids round-robin over the 8 XCDs),
+// where its query-tile stream is shared in L2.  8 waves.
 // Workgroup (kb, hk, split) sums over query heads hk*g + [split*hpb, (split+1)*hpb).
 //
 // The block's 128 keys form four groups of 32, and each group has two waves
@@ -517,10 +522,12 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int grp = wave & 3, role = wave >> 2;
   const int group = p.a_t / p.k_t;
   const int hpb = group / p.n_split;
-  const int hk = blockIdx.y / p.n_split, split = blockIdx.y % p.n_split;
-  const int bi = blockIdx.z;
+  const int nyz = p.k_t * p.n_split * p.b;
+  const int kb = static_cast<int>(blockIdx.x) / nyz, yz = static_cast<int>(blockIdx.x) % nyz;
+  const int hk = yz % (p.k_t * p.n_split) / p.n_split, split = yz % p.n_split;
+  const int bi = yz / (p.k_t * p.n_split);
   int seg, k0;
-  if (!find_tile(p, blockIdx.x, 128, seg, k0)) return;
+  if (!find_tile(p, kb, 128, seg, k0)) return;
   const KvSeg& S = p.seg[seg];
   const int my_key = k0 + grp * 32 + (lane & 31);
   const bool key_ok = my_key < S.n;
@@ -904,8 +911,8 @@ hipError_t bwd_impl(const AttnParams& p, int part, hipStream_t stream) {
     const int64_t rows = static_cast<int64_t>(p.b) * p.n_q;
     hipLaunchKernelGGL(attn_delta_kernel<D>, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, p);
   } else if (part == 1) {
-    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(count_blocks(p, 128), p.k_t * p.n_split, p.b), dim3(512), 0,
-                       stream, p);
+    const unsigned blocks = static_cast<unsigned>(count_blocks(p, 128)) * p.k_t * p.n_split * p.b;
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(blocks), dim3(512), 0, stream, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.n_split == 1) return e;
     hipLaunchKernelGGL(attn_dkv_reduce_kernel<D>, dim3(p.total_keys, p.k_t, p.b), dim3(64), 0, stream, p);
