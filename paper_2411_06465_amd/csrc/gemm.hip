@@ -66,10 +66,14 @@ __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(ui
 // LDS read of the next stage, exposing the copy latency on every stage.  The
 // kernels wait for their own copies (vmcnt) before the barrier that publishes
 // a stage, and before the stages are reused as epilogue staging space.
+// TAG only changes the asm text (a comment), to keep copies in the two arms of
+// a branch from being merged.
+template <int TAG = 0>
 __device__ __forceinline__ void dma16(const uint16_t* g, const uint8_t* lds) {
   const uint32_t l = __builtin_amdgcn_readfirstlane(   // uniform by construction; stated for the compiler
       static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LPTR(const_cast<uint8_t*>(lds)))));
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(l) : "memory", "m0");
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off ; copy form %2" ::"v"(g), "s"(l), "n"(TAG)
+               : "memory", "m0");
 }
 
 __device__ __forceinline__ u32x4 pack8(const float* v) {
@@ -704,7 +708,9 @@ __device__ __forceinline__ void copy2_kc(uint8_t* lds, const Kc2Rows<WAVES>& row
 // a uniform stride: copy q reads k-row kr0 + 2 * WAVES * q, and the column
 // swizzle depends on kr mod 4, which q does not change.  One offset per lane
 // is kept; each stage adds one uniform row offset.  A split operand resolves
-// every k-row through RowSrc.
+// every k-row through RowSrc.  The two arms issue textually different copies
+// (dma16<1> for the split one): with identical ones the compiler sinks the copy
+// below the branch and computes both addresses on every copy.
 struct Mn2Rows {
   uint32_t off0;   // element offset of the lane's 16 bytes for copy 0 at k0 = 0
 };
@@ -738,7 +744,7 @@ __device__ __forceinline__ void copy2_mn(uint8_t* lds, const Operand& op, const 
     if (x >= op.rows) x = op.rows - 8;
     const uint32_t o = op.src.row_index(k0 + kr);
     const uint16_t* base = (o & 0x80000000u) ? op.src.peer : op.src.own;
-    dma16(base + static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld + x, lds + kb * 1024);
+    dma16<1>(base + static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld + x, lds + kb * 1024);
   }
 }
 
