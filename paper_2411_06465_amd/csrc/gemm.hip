@@ -540,14 +540,17 @@ __device__ __forceinline__ void settle_acc(f32x16 (&acc)[4][NS]) {
 struct TileCoord {
   int tm, tn;
 };
-__device__ __forceinline__ TileCoord tile_of(const GemmParams& p) {
+// Tile `pid` in the grouped order: GROUP_M tile rows at a time, column by column.
+__device__ __forceinline__ TileCoord tile_coord(const GemmParams& p, int pid) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = p.B.split_rows ? (p.B.split_rows + 127) / 128 : (p.N + BN - 1) / BN;
-  const int pid = xcd_remap(blockIdx.x, gridDim.x);
   const int group = GROUP_M * tiles_n;
   const int first_m = (pid / group) * GROUP_M;
   const int gm = min(tiles_m - first_m, GROUP_M);
   return TileCoord{first_m + (pid % group) % gm, (pid % group) / gm};
+}
+__device__ __forceinline__ TileCoord tile_of(const GemmParams& p) {
+  return tile_coord(p, xcd_remap(blockIdx.x, gridDim.x));
 }
 
 // 8 waves (two per SIMD), each 128 x 64.
@@ -802,15 +805,102 @@ __device__ __forceinline__ void interleave2() {
   interleave2_slots<DS, NS / 2>();
 }
 
+// The BK = 64 main loop of one tile over its stages [kb, kb + n), n even:
+// products added into acc.  The four stage buffers a0 b0 a1 b1 (32 KB each)
+// hold two stages.  SETTLE: acc holds a C tile still being loaded (the fp32
+// accumulate), settled after the first stage's copies.
+template <Layout LA, Layout LB, int WAVES, bool SETTLE>
+__device__ __forceinline__ void mainloop64(const GemmParams& p, f32x16 (&acc)[4][WAVES == 8 ? 2 : 4], int tm, int tn,
+                                           int kb, int n, uint8_t* a0, uint8_t* b0, uint8_t* a1, uint8_t* b1,
+                                           int wave, int lane, int wm, const int* ncol) {
+  constexpr int NS = WAVES == 8 ? 2 : 4;
+  constexpr int PER = 32 / WAVES;           // copy instructions per operand per stage per wave
+  const int m0 = tm * BM, n0 = tn * BN;
+  Kc2Rows<WAVES> ra{}, rb{};
+  Mn2Rows ma{}, mb{};
+  if constexpr (LA == Layout::KC) ra = kc2_rows<WAVES>(p.A, m0, tm, wave, lane);
+  else ma = mn2_rows<WAVES>(p.A, m0, wave, lane);
+  if constexpr (LB == Layout::KC) rb = kc2_rows<WAVES>(p.B, n0, tn, wave, lane);
+  else mb = mn2_rows<WAVES>(p.B, n0, wave, lane);
+  // stage kt of the range (stages past its end repeat the last one: the wait counts stay fixed)
+  auto issue_a = [&](int kt, uint8_t* la) {
+    const int k0 = (kb + min(kt, n - 1)) * BK2;
+    if constexpr (LA == Layout::KC) copy2_kc<WAVES>(la, ra, k0, wave);
+    else copy2_mn<WAVES>(la, p.A, ma, m0, k0, wave, lane);
+  };
+  auto issue_b = [&](int kt, uint8_t* lb) {
+    const int k0 = (kb + min(kt, n - 1)) * BK2;
+    if constexpr (LB == Layout::KC) copy2_kc<WAVES>(lb, rb, k0, wave);
+    else copy2_mn<WAVES>(lb, p.B, mb, n0, k0, wave, lane);
+  };
+
+  Frags2<NS> f0, f1;
+  // Stage kt (buffers X, next stage in Y): sub-steps kk = 0..3 each read the
+  // fragments of the next sub-step under their own MFMAs.  Before the last
+  // sub-step every wave has read all of X: wait for stage kt+1, publish it
+  // with the barrier, refill X's A half with stage kt+2 and read the first
+  // fragments of Y under the last MFMAs.  The B half of stage kt+2 follows at
+  // the start of stage kt+1 (measured a few percent faster than issuing both
+  // halves at the barrier).
+  auto stage = [&](int kt, uint8_t* xa, uint8_t* xb, const uint8_t* ya, uint8_t* yb) {
+    if (kt > 0) {
+      issue_b(kt + 1, yb);   // stage kt+1's B half (Y's B buffer was freed at kt-1's barrier)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    read_frags2<LA, LB, NS>(f1, xa, xb, wm, ncol, 1, lane);
+    mfma_frags2<NS>(acc, f0);
+    interleave2<LA, LB, NS>();
+    read_frags2<LA, LB, NS>(f0, xa, xb, wm, ncol, 2, lane);
+    mfma_frags2<NS>(acc, f1);
+    interleave2<LA, LB, NS>();
+    read_frags2<LA, LB, NS>(f1, xa, xb, wm, ncol, 3, lane);
+    mfma_frags2<NS>(acc, f0);
+    interleave2<LA, LB, NS>();
+    wait_vm<0>();
+    stage_barrier();
+    issue_a(kt + 2, xa);
+    // Keep the copies here, right after the barrier: left alone, the scheduler
+    // sinks them to the end of the next stage, next to the wait for them, and
+    // no computation overlaps their latency.
+    __builtin_amdgcn_sched_barrier(0);
+    read_frags2<LA, LB, NS>(f0, ya, yb, wm, ncol, 0, lane);   // after the last stage: read, never used
+    mfma_frags2<NS>(acc, f1);
+    interleave2<LA, LB, NS>();
+  };
+
+  issue_a(0, a0);
+  issue_b(0, b0);
+  if constexpr (SETTLE) settle_acc<NS>(acc);   // the C tile (and stage 0) have landed
+  issue_a(1, a1);
+  issue_b(1, b1);
+  if constexpr (PER == 8) wait_vm<16>();
+  else wait_vm<8>();
+  stage_barrier();
+  read_frags2<LA, LB, NS>(f0, a0, b0, wm, ncol, 0, lane);
+  for (int kt = 0; kt < n; kt += 2) {
+    stage(kt, a0, b0, a1, b1);
+    stage(kt + 1, a1, b1, a0, b0);
+  }
+  wait_vm<0>();      // the last (repeated) stage copy has landed
+}
+
+// Wave-private staging space of the epilogue in the stage buffers.
+template <int WAVES>
+__device__ __forceinline__ float* stage_space(uint8_t* a0, uint8_t* b0, uint8_t* a1, uint8_t* b1, int wave) {
+  const int q = WAVES == 8 ? (wave >> 1) : wave;
+  uint8_t* mine = q == 0 ? a0 : q == 1 ? b0 : q == 2 ? a1 : b1;
+  if constexpr (WAVES == 8) mine += (wave & 1) * 16384;
+  return reinterpret_cast<float*>(mine);
+}
+
 template <Layout LA, Layout LB, EpiKind KIND, int PAIR, int WAVES>
 __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   constexpr int NS = WAVES == 8 ? 2 : 4;
-  constexpr int PER = 32 / WAVES;           // copy instructions per operand per stage per wave
   __shared__ __attribute__((aligned(16))) uint8_t a0[TILE2], b0[TILE2], a1[TILE2], b1[TILE2];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave: scalar code for wave-level decisions
   const TileCoord tc = tile_of(p);
-  const int tm = tc.tm, tn = tc.tn, m0 = tm * BM, n0 = tn * BN;
+  const int tm = tc.tm, tn = tc.tn, m0 = tm * BM;
   const int wm = WAVES == 8 ? (wave >> 2) : (wave >> 1);
   const int wn = WAVES == 8 ? (wave & 3) : (wave & 1);
   int ncol[NS];
@@ -829,83 +919,15 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
 #pragma unroll
       for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
   }
-
-  Kc2Rows<WAVES> ra{}, rb{};
-  Mn2Rows ma{}, mb{};
-  if constexpr (LA == Layout::KC) ra = kc2_rows<WAVES>(p.A, m0, tm, wave, lane);
-  else ma = mn2_rows<WAVES>(p.A, m0, wave, lane);
-  if constexpr (LB == Layout::KC) rb = kc2_rows<WAVES>(p.B, n0, tn, wave, lane);
-  else mb = mn2_rows<WAVES>(p.B, n0, wave, lane);
-  auto issue_a = [&](int k0, uint8_t* la) {
-    if constexpr (LA == Layout::KC) copy2_kc<WAVES>(la, ra, k0, wave);
-    else copy2_mn<WAVES>(la, p.A, ma, m0, k0, wave, lane);
-  };
-  auto issue_b = [&](int k0, uint8_t* lb) {
-    if constexpr (LB == Layout::KC) copy2_kc<WAVES>(lb, rb, k0, wave);
-    else copy2_mn<WAVES>(lb, p.B, mb, n0, k0, wave, lane);
-  };
-
   // K is a multiple of 2 * BK2 (the host picks this kernel only then).
-  const int nk = p.K / BK2;
-  Frags2<NS> f0, f1;
-  // Stage kt (buffers X, next stage in Y): sub-steps kk = 0..3 each read the
-  // fragments of the next sub-step under their own MFMAs.  Before the last
-  // sub-step every wave has read all of X: wait for stage kt+1, publish it
-  // with the barrier, refill X's A half with stage kt+2 and read the first
-  // fragments of Y under the last MFMAs.  The B half of stage kt+2 follows at
-  // the start of stage kt+1: all 8 waves issuing a whole stage of copies at
-  // the barrier at once fill the texture path's queue, and every wave stalls
-  // at issue with its products waiting behind.
-  auto stage = [&](int kt, uint8_t* xa, uint8_t* xb, const uint8_t* ya, uint8_t* yb) {
-    if (kt > 0) {
-      issue_b(min(kt + 1, nk - 1) * BK2, yb);   // stage kt+1's B half (Y's B buffer was freed at kt-1's barrier)
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    read_frags2<LA, LB, NS>(f1, xa, xb, wm, ncol, 1, lane);
-    mfma_frags2<NS>(acc, f0);
-    interleave2<LA, LB, NS>();
-    read_frags2<LA, LB, NS>(f0, xa, xb, wm, ncol, 2, lane);
-    mfma_frags2<NS>(acc, f1);
-    interleave2<LA, LB, NS>();
-    read_frags2<LA, LB, NS>(f1, xa, xb, wm, ncol, 3, lane);
-    mfma_frags2<NS>(acc, f0);
-    interleave2<LA, LB, NS>();
-    wait_vm<0>();
-    stage_barrier();
-    issue_a(min(kt + 2, nk - 1) * BK2, xa);
-    // Keep the copies here, right after the barrier: left alone, the scheduler
-    // sinks them to the end of the next stage, next to the wait for them, and
-    // no computation overlaps their latency.
-    __builtin_amdgcn_sched_barrier(0);
-    read_frags2<LA, LB, NS>(f0, ya, yb, wm, ncol, 0, lane);   // after the last stage: read, never used
-    mfma_frags2<NS>(acc, f1);
-    interleave2<LA, LB, NS>();
-  };
-
-  issue_a(0, a0);
-  issue_b(0, b0);
-  if constexpr (KIND == EpiKind::AccF32) settle_acc<NS>(acc);   // the C tile (and stage 0) have landed
-  issue_a(BK2, a1);
-  issue_b(BK2, b1);
-  if constexpr (PER == 8) wait_vm<16>();
-  else wait_vm<8>();
-  stage_barrier();
-  read_frags2<LA, LB, NS>(f0, a0, b0, wm, ncol, 0, lane);
-  for (int kt = 0; kt < nk; kt += 2) {
-    stage(kt, a0, b0, a1, b1);
-    stage(kt + 1, a1, b1, a0, b0);
-  }
-  wait_vm<0>();      // the last (repeated) stage copy has landed
+  mainloop64<LA, LB, WAVES, KIND == EpiKind::AccF32>(p, acc, tm, tn, 0, p.K / BK2, a0, b0, a1, b1, wave,
+                                                             lane, wm, ncol);
   if constexpr (KIND == EpiKind::AccF32) {
     acc_store_f32<NS>(acc, p, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
   } else {
     __syncthreads();   // every wave is done reading the stages
-    uint8_t* mine = (WAVES == 8 ? (wave >> 1) : wave) == 0 ? a0
-                  : (WAVES == 8 ? (wave >> 1) : wave) == 1 ? b0
-                  : (WAVES == 8 ? (wave >> 1) : wave) == 2 ? a1 : b1;
-    if constexpr (WAVES == 8) mine += (wave & 1) * 16384;
-    store_tile<KIND, PAIR, NS>(p, acc, reinterpret_cast<float*>(mine), static_cast<int64_t>(m0) + wm * 128, tn,
-                               ncol, lane);
+    store_tile<KIND, PAIR, NS>(p, acc, stage_space<WAVES>(a0, b0, a1, b1, wave), static_cast<int64_t>(m0) + wm * 128,
+                               tn, ncol, lane);
   }
 }
 
