@@ -6,7 +6,10 @@ the layer backward (which adds into fp32 weight-gradient accumulators).  The
 headline workload is the Llama-2-7B-shaped layer (h 4096, 32/32 heads,
 FFN 11008, seq 4096, micro-batch 1, TP1 CP1); the other shard shapes
 (Llama-3-8B at TP2 CP2, Llama-3-70B at TP8, the Llama-3-8B LM head at TP4)
-are reported alongside under "other_workloads".
+are reported alongside under "other_workloads", and "first_stage_1f1b" plays
+the first pipeline stage of the 70B (t, c, p) = (8, 1, 8) layout under 1F1B
+with the real kernels (10 layers x 8 micro-batches) and compares its peak live
+stash with the memory model's L layers.
 
 Throughput is model FLOPs (forward GEMMs + causal attention over the
 unmasked query/key pairs, times 3 for forward + backward) per second.  Kernel
@@ -203,6 +206,54 @@ def run_layer(w, steps, warmup, profile):
     return (t1 - t0) / steps, kernels, timed, stash
 
 
+def run_first_stage_1f1b(w):
+    """Stage 0 of the (t, c, p) layout of `w` under 1F1B with p micro-batches:
+    its L/p layers on the real shard kernels, every stash kept until its
+    micro-batch's backward.  Peak live stash bytes against the memory model."""
+    import torch
+    import paper_2411_06465_amd as L
+    import workloads as W
+    from paper_2411_06465_amd.pipeline import run_first_stage
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+    weights = {k: dev(v) for k, v in W.layer_weights(w).items()}
+    ab = W.layer_activations(w)
+    x, dy = dev(ab["x"]), dev(ab["dy"])
+    peers = {k: dev(v) for k, v in ab["peers"].items()}
+    del ab
+    grads = {k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in weights.items()}
+    model, par = L.make_model(**w.model()), L.make_parallel(**w.parallel())
+    est = L.mem_estimate(model, par)
+    fws, bws = L.l4d_layer_workspace_bytes(model, par)
+    per = est["act_bytes_per_layer"] + 4 * w.micro_batch * w.a_t * w.s_c + (1 << 16)
+    arena = L.Arena.on(torch.empty(w.n_layers * per + max(fws, bws) + (64 << 20), dtype=torch.uint8, device="cuda"))
+    layers, mbs = w.n_layers // w.pp, w.pp
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    r = run_first_stage(model, par, weights, layers, mbs, x, dy, grads, arena, peers=peers)
+    torch.cuda.synchronize()
+    sec = time.perf_counter() - t0
+    in_use = arena.stats()["in_use"]
+    arena.destroy()
+    return {
+        "workload": f"{w.name}: stage 0 of {w.pp}, {layers} layers x {mbs} micro-batches of {w.micro_batch} x "
+                    f"{w.seq} tokens (t{w.tp} c{w.cp})",
+        "peak_live_stashes": r["peak_live_stashes"],
+        "peak_stash_bytes": r["peak_formula_bytes"],
+        "model_layers_bytes": w.n_layers * r["act_bytes_per_layer"],
+        "equal": r["peak_formula_bytes"] == w.n_layers * r["act_bytes_per_layer"],
+        "model_first_stage_act_bytes": r["first_stage_act_bytes"],
+        "model_embedding_term_bytes": r["first_stage_act_bytes"] - w.n_layers * r["act_bytes_per_layer"],
+        "peak_aux_lse_bytes": r["peak_aux_bytes"],
+        "peak_padding_bytes": r["peak_padding_bytes"],
+        "arena_peak_bytes": r["arena_peak_bytes"],
+        "in_use_after": in_use,
+        "seconds": round(sec, 3),
+    }
+
+
 def run_lm(w, steps, warmup):
     import torch
     import paper_2411_06465_amd as L
@@ -355,6 +406,9 @@ def main():
         others[lw.name] = {"tflops": round(lm_flops(lw) / s3 / 1e12, 2), "ms_per_step": round(s3 * 1e3, 3),
                            "pct_of_bf16_peak": round(100 * lm_flops(lw) / s3 / 1e12 / PEAK_BF16_TFLOPS, 2)}
         out["other_workloads"] = others
+        # the paper's first-stage claim, measured: 80 layer stashes of the 70B TP8 shard
+        out["first_stage_1f1b"] = run_first_stage_1f1b(W.LLAMA3_70B_TP8)
+        torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seq)
