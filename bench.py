@@ -9,7 +9,10 @@ FFN 11008, seq 4096, micro-batch 1, TP1 CP1); the other shard shapes
 are reported alongside under "other_workloads", and "first_stage_1f1b" plays
 the first pipeline stage of the 70B (t, c, p) = (8, 1, 8) layout under 1F1B
 with the real kernels (10 layers x 8 micro-batches) and compares its peak live
-stash with the memory model's L layers.
+stash with the memory model's L layers.  "optimizer_step" times the Adam
+update of that layout's optimizer shard (the 1/(d c) of a rank's parameters
+whose fp32 master, momentum and variance it owns, d c = 4): 30 bytes of HBM
+traffic per parameter, against the HBM peak.
 
 Throughput is model FLOPs (forward GEMMs + causal attention over the
 unmasked query/key pairs, times 3 for forward + backward) per second.  Kernel
@@ -20,6 +23,7 @@ dominant kernel's launches only in the timed steps (the roofline figure).
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline] [--no-others]
     python bench.py --calibrate-copy BYTES     # a plain device copy, for HBM counter calibration
+    python bench.py --optimizer-only [--steps K] [--warmup W]   # the Adam step alone
 
 roofline.traffic is the dominant kernel's HBM bytes per launch as measured
 by rocprofv3 FETCH_SIZE + WRITE_SIZE (scaled by the counters' reading for a
@@ -94,8 +98,9 @@ def lm_flops(w):
 
 # Source file of each kernel family (for the traffic table's staleness check).
 KERNEL_SOURCE = {"gemm": "gemm.hip", "attn": "attention.hip", "rmsnorm": "rowwise.hip", "reduce": "rowwise.hip",
-                 "rope": "rowwise.hip", "xent": "rowwise.hip"}
+                 "rope": "rowwise.hip", "xent": "rowwise.hip", "adam": "optim.hip"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama2_7b_layer.txt")
+ADAM_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_adam_70b_shard.txt")
 
 
 def source_sha(kernel):
@@ -106,13 +111,13 @@ def source_sha(kernel):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(kernel):
+def measured_traffic(kernel, path=TRAFFIC_FILE):
     """HBM bytes per launch from the committed counter summary, or None when
     absent or taken on a different version of the kernel's source."""
-    if not os.path.exists(TRAFFIC_FILE):
+    if not os.path.exists(path):
         return None
     sha = source_sha(kernel)
-    with open(TRAFFIC_FILE) as f:
+    with open(path) as f:
         for line in f:
             parts = line.split()
             if len(parts) == 5 and parts[0] == "traffic" and parts[1] == kernel:
@@ -254,6 +259,50 @@ def run_first_stage_1f1b(w):
     }
 
 
+ADAM_BYTES_PER_PARAM = 30     # reads grad, master, m, v (fp32); writes master, m, v (fp32), weight (bf16)
+
+
+def run_optimizer_step(w, steps, warmup):
+    """The Adam step over one rank's optimizer shard (fp32 gradient, master,
+    momentum, variance; bf16 weight), `steps` launches after `warmup`, with
+    events around every launch on the launch stream."""
+    import torch
+    import paper_2411_06465_amd as L
+    import workloads as W
+
+    st = W.adam_inputs_device(w.name, w.n)
+    wb = torch.empty(w.n, dtype=torch.bfloat16, device="cuda")
+    hp = dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay)
+    t = w.step
+    for _ in range(warmup):
+        L.l4d_adam_step(st["grad"], st["master"], st["m"], st["v"], wb, t, **hp)
+        t += 1
+    torch.cuda.synchronize()
+    L.l4d_profile_reset()
+    L.l4d_profile_only("adam_step")
+    L.l4d_profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        L.l4d_adam_step(st["grad"], st["master"], st["m"], st["v"], wb, t, **hp)
+        t += 1
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / steps
+    L.l4d_profile_enable(False)
+    launches, ms = L.l4d_profile_read("adam_step")
+    L.l4d_profile_only(None)
+    del st, wb
+    torch.cuda.empty_cache()
+    avg_s = ms / launches / 1e3
+    gbs = ADAM_BYTES_PER_PARAM * w.n / avg_s / 1e9
+    return {"workload": f"{w.name}: {w.n} parameters, Adam step {w.step}+ (lr {w.lr}, betas ({w.beta1}, "
+                        f"{w.beta2}), eps {w.eps}, weight decay {w.weight_decay})",
+            "bytes_per_param": ADAM_BYTES_PER_PARAM, "launches": launches,
+            "kernel_ms": round(ms / launches, 4), "wall_ms_per_step": round(sec * 1e3, 4),
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "traffic": measured_traffic("adam_step", ADAM_TRAFFIC_FILE)}}
+
+
 def run_lm(w, steps, warmup):
     import torch
     import paper_2411_06465_amd as L
@@ -319,6 +368,8 @@ def main():
     ap.add_argument("--no-others", action="store_true")
     ap.add_argument("--cpu-seq", type=int, default=2048)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--optimizer-only", action="store_true",
+                    help="time only the Adam step over the 70B optimizer shard and print its object")
     args = ap.parse_args()
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
@@ -334,6 +385,10 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
+    if args.optimizer_only:
+        print(json.dumps({"optimizer_step": run_optimizer_step(W.ADAM_70B_SHARD, args.steps, args.warmup)}),
+              flush=True)
+        return
 
     w = W.LLAMA2_7B
     prof_steps = max(3, args.steps // 4)
@@ -409,6 +464,8 @@ def main():
         # the paper's first-stage claim, measured: 80 layer stashes of the 70B TP8 shard
         out["first_stage_1f1b"] = run_first_stage_1f1b(W.LLAMA3_70B_TP8)
         torch.cuda.empty_cache()
+        # the per-step optimizer update of the same layout's optimizer shard
+        out["optimizer_step"] = run_optimizer_step(W.ADAM_70B_SHARD, max(10, args.steps // 2), 3)
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seq)

@@ -246,6 +246,43 @@ int lm_head_xent(int64_t n_tokens, int64_t hidden, int64_t vocab_shard, int64_t 
                  float* loss, void* d_hidden, float* d_w_lm, l4d_arena* arena, void* hip_stream);
 
 /* ------------------------------------------------------------------------
+ * Optimizer step over one shard of the model states (Sec. 3.1, Eqs. 4-5, 10)
+ *
+ * Each GPU holds 2 bytes (bf16 weight) and 4 bytes (fp32 gradient) per
+ * parameter, plus 12 bytes of optimizer state (fp32 master weight, momentum,
+ * variance) for the 1/(d c) of its parameters that it owns under the
+ * distributed optimizer.  l4d_adam_step updates such a shard of n parameters
+ * in one pass, with the bias-corrected Adam step and decoupled weight decay:
+ *   g = grad * grad_scale [* *grad_scale_dev]
+ *   m = beta1 m + (1 - beta1) g;   v = beta2 v + (1 - beta2) g^2
+ *   master -= lr (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps)
+ *             + lr weight_decay master
+ *   weight = bf16(master), rounded to nearest even;  grad = 0 if zero_grad.
+ * Arithmetic is fp32; the step-dependent constants are formed in double.
+ *   grad, master, m, v: fp32 [n] device arrays, 16-byte aligned;
+ *   weight: bf16 [n] device array, 8-byte aligned (the shard's slice of the
+ *   full weight, which the data-parallel all-gather then distributes);
+ *   the five arrays must not overlap; all are owned by the caller.
+ * L4D_EINVAL for n < 0 or n > 2^33, a NULL or misaligned array, overlapping arrays,
+ * step < 1, beta1 or beta2 outside [0, 1), eps < 0, or a non-finite lr,
+ * weight decay or scale.  n == 0 launches nothing.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  float lr;
+  float beta1, beta2;
+  float eps;
+  float weight_decay;            /* decoupled: 0 gives plain Adam */
+  float grad_scale;              /* multiplies the gradient (1 = none) */
+  const float* grad_scale_dev;   /* optional device scalar multiplied in as well
+                                    (e.g. a clipping factor computed on the GPU) */
+  int64_t step;                  /* 1 for the first step */
+  int32_t zero_grad;             /* != 0: clear grad after reading it */
+} l4d_adam;
+
+int l4d_adam_step(const l4d_adam* hp, int64_t n, float* grad, float* master, float* m, float* v,
+                  void* weight, void* hip_stream);
+
+/* ------------------------------------------------------------------------
  * Kernel timing (HIP events around every launch, on the launch stream)
  * ---------------------------------------------------------------------- */
 

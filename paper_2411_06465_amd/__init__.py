@@ -58,6 +58,12 @@ class PeerOutputs(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in PEER_OUTPUTS]
 
 
+class Adam(C.Structure):
+    _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("weight_decay", C.c_float), ("grad_scale", C.c_float), ("grad_scale_dev", C.c_void_p),
+                ("step", C.c_int64), ("zero_grad", C.c_int32)]
+
+
 _lib = None
 
 
@@ -87,6 +93,7 @@ def lib():
                                  C.POINTER(PeerInputs), C.POINTER(PeerOutputs), P, P, P, C.POINTER(LayerGrads),
                                  P, P, P, P], C.c_int),
             "lm_head_xent": ([i64, i64, i64, i64, P, P, P, P, P, f32, P, P, P, P, P], C.c_int),
+            "l4d_adam_step": ([C.POINTER(Adam), i64, P, P, P, P, P, P], C.c_int),
             "l4d_profile_enable": ([C.c_int], C.c_int),
             "l4d_profile_only": ([C.c_char_p], C.c_int),
             "l4d_profile_read": ([C.c_char_p, C.POINTER(i64), C.POINTER(C.c_double)], C.c_int),
@@ -242,6 +249,19 @@ def lm_head_xent(hidden, w_lm, targets, loss, d_hidden, d_w_lm, arena, vocab_sta
     _check(lib().lm_head_xent(n, h, v_t, vocab_start, _ptr(hidden), _ptr(w_lm), _ptr(targets), _ptr(peer_lse),
                               _ptr(peer_target_logit), grad_scale, _ptr(loss), _ptr(d_hidden), _ptr(d_w_lm),
                               arena.h, _stream(stream)))
+
+
+# ------------------------------------------------------------------ optimizer step
+
+def l4d_adam_step(grad, master, m, v, weight, step, lr, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0,
+                  grad_scale=1.0, grad_scale_dev=None, zero_grad=False, n=None, stream=None):
+    """One Adam step over a shard: grad, master, m, v fp32 and weight bf16, all of
+    n elements (default: grad.numel()), updated in place."""
+    n = grad.numel() if n is None else n
+    hp = Adam(lr, beta1, beta2, eps, weight_decay, grad_scale,
+              None if grad_scale_dev is None else grad_scale_dev.data_ptr(), step, 1 if zero_grad else 0)
+    _check(lib().l4d_adam_step(C.byref(hp), n, _ptr(grad), _ptr(master), _ptr(m), _ptr(v), _ptr(weight),
+                               _stream(stream)))
 
 
 # ------------------------------------------------------------------ kernel timing

@@ -17,7 +17,7 @@ ARCH = "gfx950"
 FLAGS = ["-x", "hip", f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wno-unused-command-line-argument"]
-SOURCES = ["abi.cpp", "gemm.hip", "attention.hip", "rowwise.hip"]
+SOURCES = ["abi.cpp", "gemm.hip", "attention.hip", "rowwise.hip", "optim.hip"]
 
 
 def _compile(src, objdir):

@@ -935,3 +935,46 @@ extern "C" int lm_head_xent(int64_t n, int64_t h, int64_t v_t, int64_t v0, const
   return run_gemm("gemm_lm_dw", s, v_t, h, n, op(RowSrc::plain(logits, v_t), v_t), Layout::MN,
                   op(RowSrc::plain(hidden, h), h), Layout::MN, epi_acc(d_w, h));
 }
+
+// ============================================================== optimizer
+
+extern "C" int l4d_adam_step(const l4d_adam* hp, int64_t n, float* grad, float* master, float* m, float* v,
+                             void* weight, void* stream_ptr) {
+  if (!hp) return fail(L4D_EINVAL, "hyperparameters are required");
+  if (n < 0) return fail(L4D_EINVAL, "n must be >= 0");
+  if (hp->step < 1) return fail(L4D_EINVAL, "step counts from 1");
+  if (!(hp->beta1 >= 0.f && hp->beta1 < 1.f) || !(hp->beta2 >= 0.f && hp->beta2 < 1.f))
+    return fail(L4D_EINVAL, "beta1 and beta2 must lie in [0, 1)");
+  if (!(hp->eps >= 0.f) || !std::isfinite(hp->eps)) return fail(L4D_EINVAL, "eps must be finite and >= 0");
+  if (!std::isfinite(hp->lr) || !std::isfinite(hp->weight_decay) || !std::isfinite(hp->grad_scale))
+    return fail(L4D_EINVAL, "lr, weight_decay and grad_scale must be finite");
+  if (!grad || !master || !m || !v || !weight) return fail(L4D_EINVAL, "grad, master, m, v and weight are required");
+  const void* f32s[4] = {grad, master, m, v};
+  for (const void* p : f32s)
+    if (reinterpret_cast<uintptr_t>(p) % 16) return fail(L4D_EINVAL, "fp32 arrays must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(weight) % 8) return fail(L4D_EINVAL, "the weight must be 8-byte aligned");
+  if (n == 0) return L4D_OK;
+  if (n > (int64_t(1) << 33)) return fail(L4D_EINVAL, "shard too large (more than 2^33 parameters)");
+  const uintptr_t lo[5] = {(uintptr_t)grad, (uintptr_t)master, (uintptr_t)m, (uintptr_t)v, (uintptr_t)weight};
+  const uint64_t len[5] = {4ull * n, 4ull * n, 4ull * n, 4ull * n, 2ull * n};
+  for (int i = 0; i < 5; ++i)
+    for (int j = i + 1; j < 5; ++j)
+      if (lo[i] < lo[j] + len[j] && lo[j] < lo[i] + len[i]) return fail(L4D_EINVAL, "the arrays overlap");
+  const double b1 = hp->beta1, b2 = hp->beta2, t = static_cast<double>(hp->step);
+  AdamConsts c;
+  c.beta1 = hp->beta1;
+  c.beta2 = hp->beta2;
+  c.one_m_beta1 = static_cast<float>(1.0 - b1);
+  c.one_m_beta2 = static_cast<float>(1.0 - b2);
+  c.lr = hp->lr;
+  c.decay = static_cast<float>(static_cast<double>(hp->lr) * hp->weight_decay);
+  c.r1 = static_cast<float>(1.0 / -std::expm1(t * std::log(b1)));
+  c.rs2 = static_cast<float>(1.0 / std::sqrt(-std::expm1(t * std::log(b2))));
+  c.eps = hp->eps;
+  c.scale = hp->grad_scale;
+  c.scale_dev = hp->grad_scale_dev;
+  hipStream_t s = static_cast<hipStream_t>(stream_ptr);
+  return launch("adam_step", s, [&] {
+    return adam_step(c, n, grad, master, m, v, static_cast<uint16_t*>(weight), hp->zero_grad, s);
+  });
+}

@@ -177,4 +177,18 @@ hipError_t xent_rows(const uint16_t* logits, int64_t n, int32_t v_t, int64_t v0,
                      const int64_t* targets, const float* peer_lse, const float* peer_z,
                      float grad_scale, float* loss, uint16_t* dlogits, hipStream_t stream);
 
+// ---------------------------------------------------------------- optimizer
+
+// Step constants of one Adam step, prepared on the host in double precision.
+struct AdamConsts {
+  float beta1, beta2, one_m_beta1, one_m_beta2;
+  float lr, decay;           // decay = lr * weight_decay
+  float r1, rs2;             // 1 / (1 - beta1^t), 1 / sqrt(1 - beta2^t)
+  float eps, scale;
+  const float* scale_dev;    // device scalar multiplying scale, or null
+};
+// grad, master, m, v: f32 [n], 16-byte aligned; weight: bf16 [n], 8-byte aligned.
+hipError_t adam_step(const AdamConsts& c, int64_t n, float* grad, float* master, float* m, float* v,
+                     uint16_t* weight, int32_t zero_grad, hipStream_t stream);
+
 }  // namespace l4d

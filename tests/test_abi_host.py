@@ -189,3 +189,47 @@ def test_layer_calls_validate_before_touching_the_device():
     with pytest.raises(L.L4DError):
         L.l4d_layer_workspace_bytes(m2, L.make_parallel(64))
     a.destroy()
+
+
+def _adam(**kw):
+    base = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0, grad_scale=1.0,
+                grad_scale_dev=None, step=1, zero_grad=0)
+    base.update(kw)
+    return L.Adam(*[base[n] for n, _ in L.Adam._fields_])
+
+
+def _adam_rc(hp, n=1024, ptrs=None):
+    g, w, m, v, b = ptrs or (FAKE_BASE, FAKE_BASE + (1 << 20), FAKE_BASE + (2 << 20), FAKE_BASE + (3 << 20),
+                             FAKE_BASE + (4 << 20))
+    return L.lib().l4d_adam_step(C.byref(hp), n, g, w, m, v, b, None)
+
+
+def test_adam_step_validates_before_touching_the_device():
+    # every rejected call returns before any HIP call, so fake addresses are safe
+    assert _adam_rc(_adam(step=0)) == L.L4D_EINVAL
+    assert _adam_rc(_adam(beta1=1.0)) == L.L4D_EINVAL
+    assert _adam_rc(_adam(beta2=-0.1)) == L.L4D_EINVAL
+    assert _adam_rc(_adam(eps=-1e-8)) == L.L4D_EINVAL
+    assert _adam_rc(_adam(lr=float("nan"))) == L.L4D_EINVAL
+    assert _adam_rc(_adam(grad_scale=float("inf"))) == L.L4D_EINVAL
+    assert _adam_rc(_adam(), n=-1) == L.L4D_EINVAL
+    assert L.lib().l4d_adam_step(None, 4, FAKE_BASE, FAKE_BASE, FAKE_BASE, FAKE_BASE, FAKE_BASE, None) == L.L4D_EINVAL
+    base = [FAKE_BASE + (i << 20) for i in range(5)]
+    for i in range(5):
+        p = list(base)
+        p[i] = None
+        assert _adam_rc(_adam(), ptrs=p) == L.L4D_EINVAL
+        p[i] = base[i] + (4 if i < 4 else 2)          # misaligned
+        assert _adam_rc(_adam(), ptrs=p) == L.L4D_EINVAL
+    # overlapping arrays: m starts inside the master's 4n bytes
+    p = list(base)
+    p[2] = base[1] + 2048
+    assert _adam_rc(_adam(), n=1024, ptrs=p) == L.L4D_EINVAL
+    assert "overlap" in L.lib().l4d_last_error().decode()
+    # an empty shard is accepted and launches nothing
+    assert _adam_rc(_adam(), n=0) == L.L4D_OK
+
+
+def test_adam_step_rejects_oversized_shard():
+    assert _adam_rc(_adam(), n=(1 << 33) + 4) == L.L4D_EINVAL
+    assert "too large" in L.lib().l4d_last_error().decode()

@@ -97,3 +97,10 @@ def test_weight_is_the_fp32_master_on_the_bf16_grid():
 def test_step_counts_from_one():
     with pytest.raises(ValueError):
         adam_step(np.zeros(1), np.zeros(1), np.zeros(1), np.zeros(1), 0, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8)
+
+
+def test_70b_shard_size_is_the_memory_model_share():
+    # first pipeline stage of a TP rank of Llama-3-70B at (t, p) = (8, 8), over d c = 4
+    import workloads as W
+    from oracle.memory import params_per_gpu
+    assert W.ADAM_70B_SHARD.n * 4 == params_per_gpu(8192, 64, 8, 28672, 80, 128256, 8, 8)

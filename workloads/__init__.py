@@ -9,7 +9,9 @@ which is needed to exercise the arithmetic): projection weights N(0, 0.02)
 bf16; RMSNorm gains 1 + N(0, 0.02) bf16; layer inputs, upstream gradients,
 remote K/V chunks and sequence-parallel peer slices N(0, 1) bf16; target ids
 uniform over the full vocabulary; peer log-sum-exp N(12.3, 0.1) and peer
-target logits N(0, 1.28) in fp32.  Every tensor has its own stream, derived
+target logits N(0, 1.28) in fp32.  Optimizer shards (fp32): master weights
+N(0, 0.02); gradients N(0, 1) times 10^U(-4, -2), so their magnitudes span
+two decades; momentum 0.3 times such a draw; variance the square of one.  Every tensor has its own stream, derived
 from the master seed, the workload name and the tensor name.
 """
 import zlib
@@ -193,3 +195,63 @@ def lm_head_inputs(w: LMHeadWorkload):
         out["peer_lse"] = (_rng(n, "peer_lse").standard_normal(w.tokens) * 0.1 + 12.3).astype(np.float32)
         out["peer_target_logit"] = (_rng(n, "peer_z").standard_normal(w.tokens) * 1.28).astype(np.float32)
     return out
+
+
+# ---------------------------------------------------------------- optimizer shards
+
+@dataclass(frozen=True)
+class AdamWorkload:
+    """One data-parallel rank's shard of the optimizer states: n parameters,
+    stepped with the given Adam hyperparameters at step number `step`."""
+    name: str
+    n: int
+    step: int = 1000
+    lr: float = 1.5e-4
+    beta1: float = 0.9
+    beta2: float = 0.95
+    eps: float = 1e-5
+    weight_decay: float = 0.1
+
+
+def _grad_like(r, n):
+    g = r.standard_normal(n, dtype=np.float32)
+    g *= (10.0 ** r.uniform(-4.0, -2.0, n)).astype(np.float32)
+    return g
+
+
+def adam_inputs(name, n):
+    """fp32 arrays grad, master, m, v of n elements for the shard `name`."""
+    master = _rng(name, "master").standard_normal(n, dtype=np.float32)
+    master *= np.float32(0.02)
+    m = _grad_like(_rng(name, "m"), n)
+    m *= np.float32(0.3)
+    v = _grad_like(_rng(name, "v"), n)
+    v *= v
+    return dict(grad=_grad_like(_rng(name, "grad"), n), master=master, m=m, v=v)
+
+
+def adam_inputs_device(name, n, device="cuda"):
+    """The same distributions as adam_inputs, drawn on the GPU by torch's
+    seeded generator (a different stream of numbers: for shards of hundreds
+    of millions of parameters, where host draws would take minutes)."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(zlib.crc32(f"{SEED}:{name}".encode()))
+
+    def grad_like():
+        g = torch.randn(n, generator=gen, device=device, dtype=torch.float32)
+        g *= torch.pow(10.0, torch.rand(n, generator=gen, device=device, dtype=torch.float32) * 2.0 - 4.0)
+        return g
+
+    master = torch.randn(n, generator=gen, device=device, dtype=torch.float32) * 0.02
+    m = grad_like() * 0.3
+    v = grad_like()
+    v *= v
+    return dict(grad=grad_like(), master=master, m=m, v=v)
+
+
+# The optimizer shard of one rank of Llama-3-70B at (TP, CP, PP, DP) = (8, 1, 8, 4)
+# on 256 GPUs: the parameters of the first pipeline stage of a tensor-parallel
+# rank (1,201,045,504: the LM-head shard and 10 layers), divided over the
+# d c = 4 ranks that share the optimizer states.
+ADAM_70B_SHARD = AdamWorkload("llama3-70b-tp8pp8dp4-optimizer-shard", 300_261_376)
