@@ -76,3 +76,13 @@ def gib_2dp(n_bytes):
     if q - n >= Fr(1, 2):
         n += 1
     return Fr(n, 100)
+
+
+def oom_class(total_bytes, device_bytes):
+    """The paper's reading of an estimate against the device memory (Sec. 4.1):
+    at most 80 % of it -> "green" (trainable: temporary buffers and
+    fragmentation fit in the remaining 20 %), at most all of it -> "yellow"
+    (may or may not run out of memory), above it -> "red" (out of memory)."""
+    if Fr(total_bytes) <= Fr(8, 10) * device_bytes:
+        return "green"
+    return "yellow" if Fr(total_bytes) <= device_bytes else "red"

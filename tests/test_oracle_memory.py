@@ -162,3 +162,37 @@ def test_gib_rounding():
     assert M.gib_2dp(1 << 30) == 1
     assert M.gib_2dp(-(-(1 << 30) * 5 // 1000)) == Fr(1, 100)   # just above 0.005 GiB rounds up
     assert M.gib_2dp((1 << 30) * 4 // 1000) == 0
+
+
+OUTCOMES = os.path.join(os.path.dirname(__file__), "golden", "paper_oom_outcomes.json")
+
+
+def test_oom_outcomes_replay_the_80_percent_rule():
+    # Sec. 4.1: the five throughput tables colour each run by the estimate and
+    # print OOM where training ran out of memory.  The rule must give every
+    # printed colour, every green run must have trained and every red one must
+    # have run out of memory; yellow runs may go either way.
+    with open(OUTCOMES) as f:
+        runs = json.load(f)["cells"]
+    assert len(runs) == 454
+    seen = {}
+    for c in runs:
+        got = M.oom_class(estimate_cell(c)["total"], c["gpu_mem_gb"] << 30)
+        assert got == c["colour"], key(c)
+        oom = c["printed"] == "OOM"
+        if not oom:
+            float(c["printed"])
+        seen[(got, oom)] = seen.get((got, oom), 0) + 1
+    assert ("green", True) not in seen and ("red", False) not in seen
+    assert seen == {("green", False): 207, ("red", True): 171, ("yellow", True): 42, ("yellow", False): 34}
+
+
+def test_oom_class_boundaries():
+    gib = 1 << 30
+    assert M.oom_class(32 * gib, 40 * gib) == "green"
+    assert M.oom_class(32 * gib + 1, 40 * gib) == "yellow"
+    assert M.oom_class(40 * gib, 40 * gib) == "yellow"
+    assert M.oom_class(40 * gib + 1, 40 * gib) == "red"
+    # the closest printed runs to the 80% line sit just under it and trained
+    assert M.oom_class(M.estimate(4096, 32, 8, 14336, 32, 128256, s=8192, b=2, t=4, c=1, p=2,
+                                  n_gpus=16)["total"], 40 * gib) == "green"
