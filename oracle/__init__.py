@@ -12,7 +12,9 @@ Modules
   layer    -- one GPU's shard of a Llama decoder layer, forward and backward,
               float64 numpy with bf16 rounding at the tensors the layer stores
   lm_head  -- the tensor-parallel LM head with vocabulary-parallel cross-entropy
+  ends     -- the vocabulary-parallel embedding and the LM-head block (final
+              RMSNorm, linear, FP32 softmax cross-entropy), forward and backward
   optim    -- one Adam step over a shard of the 18-bytes-per-parameter layout
   bf16     -- round-to-nearest-even onto the bfloat16 grid (the oracle's own)
 """
-from . import bf16, memory, layer, lm_head, optim  # noqa: F401
+from . import bf16, memory, layer, lm_head, ends, optim  # noqa: F401
