@@ -12,7 +12,10 @@ with the real kernels (10 layers x 8 micro-batches) and compares its peak live
 stash with the memory model's L layers.  "optimizer_step" times the Adam
 update of that layout's optimizer shard (the 1/(d c) of a rank's parameters
 whose fp32 master, momentum and variance it owns, d c = 4): 30 bytes of HBM
-traffic per parameter, against the HBM peak.
+traffic per parameter, against the HBM peak.  "model_ends" times the LM-head
+block (final RMSNorm, FP32 logits kept as the softmax, cross-entropy, forward
+and backward) and the embedding of the Llama-3-8B TP4 rank, with their stash
+bytes against the LM-head and embedding terms of the memory model.
 
 Throughput is model FLOPs (forward GEMMs + causal attention over the
 unmasked query/key pairs, times 3 for forward + backward) per second.  Kernel
@@ -303,6 +306,80 @@ def run_optimizer_step(w, steps, warmup):
                          "traffic": measured_traffic("adam_step", ADAM_TRAFFIC_FILE)}}
 
 
+def run_model_ends(w, steps, warmup):
+    """The LM-head block (final RMSNorm, FP32 logits, cross-entropy; forward +
+    backward) and the vocabulary-parallel embedding (forward + backward) of one
+    rank, timed over `steps` after `warmup`, with their stash bytes against the
+    activation terms of the memory model."""
+    import torch
+    import paper_2411_06465_amd as L
+    import workloads as W
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+    inp = W.ends_inputs(w)
+    model, par = L.make_model(**w.model()), L.make_parallel(**w.parallel())
+    buf = torch.empty(2 * w.tokens * w.v_t * 4 + 16 * w.tokens * w.hidden + (64 << 20), dtype=torch.uint8,
+                      device="cuda")
+    arena = L.Arena.on(buf)
+    x, wn, wl = dev(inp["x"]), dev(inp["w_norm"]), dev(inp["w_lm"])
+    tg = torch.from_numpy(inp["targets"]).cuda()
+    peer_xn = dev(inp["peer_xn"]) if w.tp > 1 else None
+    pl = torch.from_numpy(inp["peer_lse"]).cuda() if w.tp > 1 else None
+    pz = torch.from_numpy(inp["peer_target_logit"]).cuda() if w.tp > 1 else None
+    pdxn = dev(inp["peer_dxn"]) if w.tp > 1 else None
+    loss = torch.empty(w.tokens, dtype=torch.float32, device="cuda")
+    dx = torch.empty_like(x)
+    dgn = torch.zeros(w.hidden, dtype=torch.float32, device="cuda")
+    dwl = torch.zeros((w.v_t, w.hidden), dtype=torch.float32, device="cuda")
+    send = torch.empty((w.micro_batch, (w.tp - 1) * w.s_sp, w.hidden), dtype=torch.bfloat16,
+                       device="cuda") if w.tp > 1 else None
+    ids = torch.from_numpy(inp["ids"]).cuda()
+    we = dev(inp["w_emb"])
+    xe = torch.empty_like(x)
+    rc = dev(inp["emb_receipt"]) if w.tp > 1 else None
+    dxe = dev(inp["dx_emb"])
+    pdxe = dev(inp["peer_dx_emb"]) if w.tp > 1 else None
+    dwe = torch.zeros((w.v_t, w.hidden), dtype=torch.float32, device="cuda")
+    sizes = {}
+
+    def head():
+        st = L.lm_head_fwd(model, par, x, wn, wl, tg, loss, arena, peer_xn=peer_xn, peer_lse=pl,
+                           peer_target_logit=pz)
+        sizes["head"] = st.bytes()["formula"]
+        L.lm_head_bwd(model, par, wn, wl, tg, st, dx, dgn, dwl, arena, grad_scale=1.0 / w.tokens,
+                      peer_xn=peer_xn, peer_dxn=pdxn, dxn_send=send)
+
+    def emb():
+        st = L.embedding_fwd(model, par, ids, we, xe, arena, receipt=rc, send=send)
+        sizes["emb"] = st.bytes()["formula"]
+        L.embedding_bwd(model, par, st, dxe, dwe, arena, peer_dx=pdxe)
+
+    out = {}
+    for name, fn in (("lm_head_block", head), ("embedding", emb)):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        out[name] = (time.perf_counter() - t0) / steps
+    arena.destroy()
+    flops = 3 * 2 * w.tokens * w.v_t * w.hidden
+    sbh_tc = w.seq * w.micro_batch * w.hidden // (w.tp * w.cp)
+    return {"workload": f"{w.name}: {w.tokens} tokens, hidden {w.hidden}, vocabulary shard {w.v_t} of {w.vocab} "
+                        f"(t{w.tp} c{w.cp})",
+            "lm_head_block_ms": round(out["lm_head_block"] * 1e3, 4),
+            "lm_head_block_tflops": round(flops / out["lm_head_block"] / 1e12, 1),
+            "lm_head_stash_bytes": sizes["head"],
+            "model_lm_head_term_bytes": 4 * sbh_tc * (w.hidden + w.vocab) // w.hidden,
+            "embedding_ms": round(out["embedding"] * 1e3, 4),
+            "embedding_stash_bytes": sizes["emb"],
+            "model_embedding_term_bytes_per_micro_batch": 8 * sbh_tc}
+
+
 def run_lm(w, steps, warmup):
     import torch
     import paper_2411_06465_amd as L
@@ -463,6 +540,9 @@ def main():
         out["other_workloads"] = others
         # the paper's first-stage claim, measured: 80 layer stashes of the 70B TP8 shard
         out["first_stage_1f1b"] = run_first_stage_1f1b(W.LLAMA3_70B_TP8)
+        torch.cuda.empty_cache()
+        # the ends of the model: LM-head block with its FP32 softmax stash, and the embedding
+        out["model_ends"] = run_model_ends(W.ENDS_LLAMA3_8B_TP4, max(5, args.steps // 2), 2)
         torch.cuda.empty_cache()
         # the per-step optimizer update of the same layout's optimizer shard
         out["optimizer_step"] = run_optimizer_step(W.ADAM_70B_SHARD, max(10, args.steps // 2), 3)

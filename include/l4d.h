@@ -138,11 +138,14 @@ enum {
  * itself; exposed for accounting).  L4D_ENOMEM if it does not fit. */
 int l4d_stash_reserve(l4d_arena* arena, const l4d_model* model, const l4d_parallel* par,
                       l4d_stash** out);
-/* formula_bytes: sum of the 12 bf16 stash tensors, equal to Eq. 12 / (tc).
- * aux_bytes: the LSE buffer.  padding_bytes: alignment gaps inside the arena. */
+/* formula_bytes: sum of the 12 bf16 stash tensors, equal to Eq. 12 / (tc)
+ * (LM-head stash: x, xn and the softmax, the LM-head term / (tc); embedding
+ * stash: the int64 ids).  aux_bytes: the LSE buffer (0 for the ends).
+ * padding_bytes: alignment gaps inside the arena. */
 int l4d_stash_bytes(const l4d_stash* stash, uint64_t* formula_bytes, uint64_t* aux_bytes,
                     uint64_t* padding_bytes);
-/* Device address and byte size of one stashed tensor (L4D_STASH_*). */
+/* Device address and byte size of one stashed tensor (L4D_STASH_* for a layer
+ * stash, L4D_HEAD_* / L4D_EMB_* for the stashes of the model's ends). */
 int l4d_stash_tensor(const l4d_stash* stash, int which, void** ptr, uint64_t* bytes);
 /* Return a stash to its arena without running the backward. */
 int l4d_stash_release(l4d_arena* arena, l4d_stash* stash);
@@ -255,6 +258,62 @@ int lm_head_xent(int64_t n_tokens, int64_t hidden, int64_t vocab_shard, int64_t 
                  const void* hidden_states, const void* w_lm, const int64_t* targets,
                  const float* peer_lse, const float* peer_target_logit, float grad_scale,
                  float* loss, void* d_hidden, float* d_w_lm, l4d_arena* arena, void* hip_stream);
+
+/* ------------------------------------------------------------------------
+ * The ends of the model (Sec. 3.2: the embedding and LM-head activation terms)
+ *
+ * Vocabulary-parallel embedding.  Rank tp_rank holds rows [v0, v0 + v_t) of
+ * the table, v_t = v/t, v0 = tp_rank v_t.  For each of its CP chunk's b*s_c
+ * tokens it produces the table row when the id is in range and zeros
+ * otherwise; the TP reduce-scatter (sequence parallelism) is explicit:
+ *   ids: int64 [b][s_c] device array of global ids in [0, v);
+ *   w_emb: bf16 [v_t][h];  receipt: bf16 [b][s_sp][h], the sum of the peers'
+ *   partial rows for this rank's rows (NULL = zero);  send: bf16
+ *   [b][(t-1) s_sp][h], this rank's partial rows for the peers in rank order
+ *   (NULL iff t == 1);  x_out: bf16 [b][s_sp][h], the own rows.
+ * The stash keeps the int64 ids (8 b s_c bytes, slot L4D_EMB_IDS): the
+ * backward needs nothing else.  The embedding term printed in Sec. 3.2,
+ * 8sbhp/(tc), counts 8sbh bytes per micro-batch: h/t times these.
+ * embedding_bwd adds, for every token whose id is in range, the all-gathered
+ * output gradient (own rows dx: bf16 [b][s_sp][h]; peer rows peer_dx: bf16
+ * [b][(t-1) s_sp][h], NULL iff t == 1) into d_w_emb: f32 [v_t][h], with fp32
+ * atomic adds (tokens sharing an id add in no fixed order).  It releases the
+ * stash.
+ *
+ * LM-head block: xn = RMSNorm(x; w_norm) on the own rows, all-gathered,
+ * logits = xn W_lm^T in FP32 over the vocabulary shard, cross-entropy with
+ * the other shards' statistics as inputs (as lm_head_xent), the FP32 softmax
+ * kept for the backward.  The stash holds exactly the LM-head term of
+ * Sec. 3.2 divided by tc: x and xn (bf16 [b][s_sp][h] each: "2sbh for the
+ * output RMSNorm" and "2sbh for the output linear layer") and the softmax
+ * (f32 [b*s_c][v_t]: "4sbv"), i.e. 4 s_c b h (1 + v/h) / t bytes.
+ *   x: bf16 [b][s_sp][h], the last layer's output (own rows);
+ *   w_norm: bf16 [h];  w_lm: bf16 [v_t][h];  targets: int64 [b*s_c];
+ *   peer_xn: bf16 [b][(t-1) s_sp][h], the peers' normed rows (NULL iff t == 1);
+ *   peer_lse, peer_target_logit: f32 [b*s_c] (NULL iff t == 1);  loss: f32 [b*s_c].
+ * lm_head_bwd takes the same weights, targets and peer_xn (the re-gather),
+ *   peer_dxn: bf16 [b][s_sp][h], the peers' partial d(xn) for the own rows
+ *   (NULL = zero);  dxn_send: bf16 [b][(t-1) s_sp][h] or NULL (then dropped);
+ *   dx: bf16 [b][s_sp][h];  d_w_norm: f32 [h] (+=);  d_w_lm: f32 [v_t][h] (+=);
+ * with dlogits = (softmax - onehot) * grad_scale, and releases the stash.
+ * Requirements: v % t == 0, (v/t) % 8 == 0, h % 8 == 0.
+ * ---------------------------------------------------------------------- */
+enum { L4D_EMB_IDS = 0, L4D_EMB_COUNT };
+enum { L4D_HEAD_X = 0, L4D_HEAD_XN, L4D_HEAD_PROBS, L4D_HEAD_COUNT };
+
+int embedding_fwd(const l4d_model* model, const l4d_parallel* par, const int64_t* ids, const void* w_emb,
+                  const void* receipt, void* send, void* x_out, l4d_arena* arena, l4d_stash** stash_out,
+                  void* hip_stream);
+int embedding_bwd(const l4d_model* model, const l4d_parallel* par, l4d_stash* stash, const void* dx,
+                  const void* peer_dx, float* d_w_emb, l4d_arena* arena, void* hip_stream);
+int lm_head_fwd(const l4d_model* model, const l4d_parallel* par, const void* x, const void* w_norm,
+                const void* w_lm, const int64_t* targets, const void* peer_xn, const float* peer_lse,
+                const float* peer_target_logit, float* loss, l4d_arena* arena, l4d_stash** stash_out,
+                void* hip_stream);
+int lm_head_bwd(const l4d_model* model, const l4d_parallel* par, const void* w_norm, const void* w_lm,
+                const int64_t* targets, const void* peer_xn, const void* peer_dxn, void* dxn_send,
+                float grad_scale, l4d_stash* stash, void* dx, float* d_w_norm, float* d_w_lm, l4d_arena* arena,
+                void* hip_stream);
 
 /* ------------------------------------------------------------------------
  * Optimizer step over one shard of the model states (Sec. 3.1, Eqs. 4-5, 10)

@@ -13,6 +13,8 @@ LIB_PATH = os.path.join(_HERE, "libl4d.so")
 
 L4D_OK, L4D_EINVAL, L4D_ENOMEM, L4D_EDEVICE = 0, 1, 2, 3
 STASH_NAMES = ["x", "xn1", "q", "k", "v", "ctx", "h1", "xn2", "gate", "up", "act", "prod", "lse"]
+HEAD_STASH_NAMES = ["x", "xn", "probs"]
+EMB_STASH_NAMES = ["ids"]
 
 
 class L4DError(RuntimeError):
@@ -95,6 +97,12 @@ def lib():
                                  P, P, P, P], C.c_int),
             "lm_head_xent": ([i64, i64, i64, i64, P, P, P, P, P, f32, P, P, P, P, P], C.c_int),
             "l4d_adam_step": ([C.POINTER(Adam), i64, P, P, P, P, P, P], C.c_int),
+            "embedding_fwd": ([C.POINTER(Model), C.POINTER(Parallel), P, P, P, P, P, P, C.POINTER(P), P], C.c_int),
+            "embedding_bwd": ([C.POINTER(Model), C.POINTER(Parallel), P, P, P, P, P, P], C.c_int),
+            "lm_head_fwd": ([C.POINTER(Model), C.POINTER(Parallel), P, P, P, P, P, P, P, P, P, C.POINTER(P), P],
+                            C.c_int),
+            "lm_head_bwd": ([C.POINTER(Model), C.POINTER(Parallel), P, P, P, P, P, P, f32, P, P, P, P, P, P],
+                            C.c_int),
             "l4d_profile_enable": ([C.c_int], C.c_int),
             "l4d_profile_only": ([C.c_char_p], C.c_int),
             "l4d_profile_read": ([C.c_char_p, C.POINTER(i64), C.POINTER(C.c_double)], C.c_int),
@@ -180,8 +188,8 @@ class Arena:
 
 
 class Stash:
-    def __init__(self, handle, arena):
-        self.h, self.arena = handle, arena
+    def __init__(self, handle, arena, names=STASH_NAMES):
+        self.h, self.arena, self.names = handle, arena, names
 
     def bytes(self):
         f, a, p = C.c_uint64(), C.c_uint64(), C.c_uint64()
@@ -191,7 +199,7 @@ class Stash:
     def tensor(self, which):
         """(device address, bytes) of stashed tensor `which` (index or name)."""
         if isinstance(which, str):
-            which = STASH_NAMES.index(which)
+            which = self.names.index(which)
         ptr, n = C.c_void_p(), C.c_uint64()
         _check(lib().l4d_stash_tensor(self.h, which, C.byref(ptr), C.byref(n)))
         return ptr.value, n.value
@@ -262,6 +270,40 @@ def lm_head_xent(hidden, w_lm, targets, loss, d_hidden, d_w_lm, arena, vocab_sta
     _check(lib().lm_head_xent(n, h, v_t, vocab_start, _ptr(hidden), _ptr(w_lm), _ptr(targets), _ptr(peer_lse),
                               _ptr(peer_target_logit), grad_scale, _ptr(loss), _ptr(d_hidden), _ptr(d_w_lm),
                               arena.h, _stream(stream)))
+
+
+# ------------------------------------------------------------------ the ends of the model
+
+def embedding_fwd(model, par, ids, w_emb, x_out, arena, receipt=None, send=None, stream=None):
+    """Vocabulary-parallel lookup of the rank's b*s_c tokens; returns the Stash (the ids)."""
+    st = C.c_void_p()
+    _check(lib().embedding_fwd(C.byref(model), C.byref(par), _ptr(ids), _ptr(w_emb), _ptr(receipt), _ptr(send),
+                               _ptr(x_out), arena.h, C.byref(st), _stream(stream)))
+    return Stash(st, arena, EMB_STASH_NAMES)
+
+
+def embedding_bwd(model, par, stash, dx, d_w_emb, arena, peer_dx=None, stream=None):
+    _check(lib().embedding_bwd(C.byref(model), C.byref(par), stash.h, _ptr(dx), _ptr(peer_dx), _ptr(d_w_emb),
+                               arena.h, _stream(stream)))
+    stash.h = None
+
+
+def lm_head_fwd(model, par, x, w_norm, w_lm, targets, loss, arena, peer_xn=None, peer_lse=None,
+                peer_target_logit=None, stream=None):
+    """Final RMSNorm, logits (FP32) and cross-entropy; returns the Stash (x, xn, softmax)."""
+    st = C.c_void_p()
+    _check(lib().lm_head_fwd(C.byref(model), C.byref(par), _ptr(x), _ptr(w_norm), _ptr(w_lm), _ptr(targets),
+                             _ptr(peer_xn), _ptr(peer_lse), _ptr(peer_target_logit), _ptr(loss), arena.h,
+                             C.byref(st), _stream(stream)))
+    return Stash(st, arena, HEAD_STASH_NAMES)
+
+
+def lm_head_bwd(model, par, w_norm, w_lm, targets, stash, dx, d_w_norm, d_w_lm, arena, grad_scale=1.0,
+                peer_xn=None, peer_dxn=None, dxn_send=None, stream=None):
+    _check(lib().lm_head_bwd(C.byref(model), C.byref(par), _ptr(w_norm), _ptr(w_lm), _ptr(targets), _ptr(peer_xn),
+                             _ptr(peer_dxn), _ptr(dxn_send), grad_scale, stash.h, _ptr(dx), _ptr(d_w_norm),
+                             _ptr(d_w_lm), arena.h, _stream(stream)))
+    stash.h = None
 
 
 # ------------------------------------------------------------------ optimizer step

@@ -384,12 +384,16 @@ int64_t qkv_cols(const Shard& x) { return (x.a_t + 2 * x.k_t) * x.d; }
 
 // ============================================================== stash
 
+enum StashKind { kLayerStash = 0, kHeadStash = 1, kEmbStash = 2 };
+
 struct l4d_stash {
   l4d_arena* arena;
   uint64_t block_off, block_size;
   uint64_t off[L4D_STASH_COUNT], bytes[L4D_STASH_COUNT];
   uint64_t formula, aux, padding;
   Shard shape;
+  int kind = kLayerStash;
+  int count = L4D_STASH_COUNT;
 };
 
 namespace {
@@ -402,19 +406,24 @@ void stash_sizes(const Shard& x, uint64_t* bytes) {
   bytes[L4D_STASH_LSE] = x.b * x.a_t * x.s_c * 4;
 }
 
-int stash_reserve(l4d_arena* A, const Shard& x, l4d_stash** out) {
+// One arena block holding `count` tensors of the given sizes, 256-byte aligned;
+// the tensor `aux_slot` (or none, -1) is reported as aux, the rest as formula.
+int stash_reserve_sized(l4d_arena* A, const Shard& x, int kind, int count, const uint64_t* bytes, int aux_slot,
+                        l4d_stash** out) {
   auto* st = new l4d_stash();
   st->arena = A;
   st->shape = x;
-  stash_sizes(x, st->bytes);
+  st->kind = kind;
+  st->count = count;
   uint64_t total = 0, raw = 0;
-  for (int i = 0; i < L4D_STASH_COUNT; ++i) {
+  for (int i = 0; i < count; ++i) {
+    st->bytes[i] = bytes[i];
     st->off[i] = total;
     total += align_up(st->bytes[i]);
-    if (i != L4D_STASH_LSE) raw += st->bytes[i];
+    if (i != aux_slot) raw += st->bytes[i];
   }
   st->formula = raw;
-  st->aux = st->bytes[L4D_STASH_LSE];
+  st->aux = aux_slot >= 0 ? st->bytes[aux_slot] : 0;
   st->padding = total - raw - st->aux;
   if (!arena_alloc(A, total, &st->block_off)) {
     delete st;
@@ -425,6 +434,12 @@ int stash_reserve(l4d_arena* A, const Shard& x, l4d_stash** out) {
   A->live.insert(st);
   *out = st;
   return L4D_OK;
+}
+
+int stash_reserve(l4d_arena* A, const Shard& x, l4d_stash** out) {
+  uint64_t bytes[L4D_STASH_COUNT];
+  stash_sizes(x, bytes);
+  return stash_reserve_sized(A, x, kLayerStash, L4D_STASH_COUNT, bytes, L4D_STASH_LSE, out);
 }
 
 template <class T = uint16_t>
@@ -451,7 +466,7 @@ extern "C" int l4d_stash_bytes(const l4d_stash* st, uint64_t* formula, uint64_t*
 
 extern "C" int l4d_stash_tensor(const l4d_stash* st, int which, void** ptr, uint64_t* bytes) {
   if (!st) return fail(L4D_EINVAL, "stash is NULL");
-  if (which < 0 || which >= L4D_STASH_COUNT) return fail(L4D_EINVAL, "no stash tensor %d", which);
+  if (which < 0 || which >= st->count) return fail(L4D_EINVAL, "no stash tensor %d", which);
   if (ptr) *ptr = sptr<void>(st, which);
   if (bytes) *bytes = st->bytes[which];
   return L4D_OK;
@@ -791,6 +806,7 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
     return fail(L4D_EINVAL, "all six gradient accumulators are required");
   if (!st || !A || !dy || !dx) return fail(L4D_EINVAL, "stash, arena, dy and dx are required");
   if (st->arena != A || !A->live.count(st)) return fail(L4D_EINVAL, "stash does not belong to this arena");
+  if (st->kind != kLayerStash) return fail(L4D_EINVAL, "not a layer stash");
   const Shard& sx = st->shape;
   if (sx.h != x.h || sx.a != x.a || sx.k != x.k || sx.f != x.f || sx.s != x.s || sx.b != x.b || sx.t != x.t ||
       sx.c != x.c || sx.tr != x.tr || sx.cr != x.cr)
@@ -942,6 +958,176 @@ extern "C" int lm_head_xent(int64_t n, int64_t h, int64_t v_t, int64_t v0, const
     return rc;
   return run_gemm("gemm_lm_dw", s, v_t, h, n, op(RowSrc::plain(logits, v_t), v_t), Layout::MN,
                   op(RowSrc::plain(hidden, h), h), Layout::MN, epi_acc(d_w, h));
+}
+
+// ============================================================== the ends of the model
+
+namespace {
+bool same_shard(const Shard& a, const Shard& b) {
+  return a.h == b.h && a.a == b.a && a.k == b.k && a.f == b.f && a.s == b.s && a.b == b.b && a.t == b.t &&
+         a.c == b.c && a.tr == b.tr && a.cr == b.cr;
+}
+
+int check_ends_stash(l4d_arena* A, const l4d_stash* st, int kind, const Shard& x) {
+  if (!st || !A) return fail(L4D_EINVAL, "stash and arena are required");
+  if (st->arena != A || !A->live.count(st)) return fail(L4D_EINVAL, "stash does not belong to this arena");
+  if (st->kind != kind) return fail(L4D_EINVAL, kind == kHeadStash ? "not an LM-head stash" : "not an embedding stash");
+  if (!same_shard(st->shape, x)) return fail(L4D_EINVAL, "stash was made for another shape");
+  return L4D_OK;
+}
+
+// Vocabulary shard of this TP rank; v % t and (v/t) % 8 are required.
+int vocab_shard(const l4d_model* m, const Shard& x, int64_t* v_t, int64_t* v0) {
+  if (m->vocab % x.t) return fail(L4D_EINVAL, "vocab %% tp != 0");
+  *v_t = m->vocab / x.t;
+  if (*v_t % 8) return fail(L4D_EINVAL, "vocab / tp must be a multiple of 8");
+  if ((int64_t)x.b * x.s_c * *v_t > ((int64_t)1 << 40)) return fail(L4D_EINVAL, "problem too large");
+  *v0 = x.tr * *v_t;
+  return L4D_OK;
+}
+}  // namespace
+
+extern "C" int embedding_fwd(const l4d_model* m, const l4d_parallel* p, const int64_t* ids, const void* w_emb,
+                             const void* receipt, void* send, void* x_out, l4d_arena* A, l4d_stash** stash_out,
+                             void* stream_ptr) {
+  Shard x;
+  int rc = make_shard(m, p, &x);
+  if (rc) return rc;
+  int64_t v_t, v0;
+  if ((rc = vocab_shard(m, x, &v_t, &v0))) return rc;
+  if (!ids || !w_emb || !x_out || !A || !stash_out) return fail(L4D_EINVAL, "ids, w_emb, x_out, arena and stash_out are required");
+  if ((x.t > 1) != (send != nullptr)) return fail(L4D_EINVAL, "send is required iff tp > 1");
+  hipStream_t s = static_cast<hipStream_t>(stream_ptr);
+  const uint64_t bytes[1] = {(uint64_t)x.b * x.s_c * 8};
+  l4d_stash* st = nullptr;
+  if ((rc = stash_reserve_sized(A, x, kEmbStash, L4D_EMB_COUNT, bytes, -1, &st))) return rc;
+  auto body = [&]() -> int {
+    HIP_TRY(hipMemcpyAsync(sptr<void>(st, L4D_EMB_IDS), ids, bytes[0], hipMemcpyDeviceToDevice, s));
+    return launch("embed_fwd", s, [&] {
+      return embed_fwd(ids, static_cast<const uint16_t*>(w_emb), v0, (int32_t)v_t, (int32_t)x.h, x.b * x.s_c,
+                       (int32_t)x.s_c, (int32_t)x.s_sp, (int32_t)x.tr, (int32_t)x.t,
+                       static_cast<const uint16_t*>(receipt), static_cast<uint16_t*>(x_out),
+                       static_cast<uint16_t*>(send), s);
+    });
+  };
+  if ((rc = body())) {
+    l4d_stash_release(A, st);
+    return rc;
+  }
+  *stash_out = st;
+  return L4D_OK;
+}
+
+extern "C" int embedding_bwd(const l4d_model* m, const l4d_parallel* p, l4d_stash* st, const void* dx,
+                             const void* peer_dx, float* d_w_emb, l4d_arena* A, void* stream_ptr) {
+  Shard x;
+  int rc = make_shard(m, p, &x);
+  if (rc) return rc;
+  int64_t v_t, v0;
+  if ((rc = vocab_shard(m, x, &v_t, &v0))) return rc;
+  if ((rc = check_ends_stash(A, st, kEmbStash, x))) return rc;
+  if (!dx || !d_w_emb) return fail(L4D_EINVAL, "dx and d_w_emb are required");
+  if ((x.t > 1) != (peer_dx != nullptr)) return fail(L4D_EINVAL, "peer_dx is required iff tp > 1");
+  hipStream_t s = static_cast<hipStream_t>(stream_ptr);
+  if ((rc = launch("embed_bwd", s, [&] {
+         return embed_bwd(sptr<const int64_t>(st, L4D_EMB_IDS), gathered(dx, peer_dx, x), v0, (int32_t)v_t,
+                          (int32_t)x.h, x.b * x.s_c, d_w_emb, s);
+       })))
+    return rc;
+  return l4d_stash_release(A, st);
+}
+
+extern "C" int lm_head_fwd(const l4d_model* m, const l4d_parallel* p, const void* x_in, const void* w_norm,
+                           const void* w_lm, const int64_t* targets, const void* peer_xn, const float* peer_lse,
+                           const float* peer_z, float* loss, l4d_arena* A, l4d_stash** stash_out, void* stream_ptr) {
+  Shard x;
+  int rc = make_shard(m, p, &x);
+  if (rc) return rc;
+  int64_t v_t, v0;
+  if ((rc = vocab_shard(m, x, &v_t, &v0))) return rc;
+  if (!x_in || !w_norm || !w_lm || !targets || !loss || !A || !stash_out)
+    return fail(L4D_EINVAL, "x, w_norm, w_lm, targets, loss, arena and stash_out are required");
+  if (x.t > 1 && (!peer_xn || !peer_lse || !peer_z))
+    return fail(L4D_EINVAL, "tp > 1 needs peer_xn, peer_lse and peer_target_logit");
+  hipStream_t s = static_cast<hipStream_t>(stream_ptr);
+  const int64_t tok = x.b * x.s_c;
+  const uint64_t sp = (uint64_t)x.b * x.s_sp * x.h * 2;
+  const uint64_t bytes[L4D_HEAD_COUNT] = {sp, sp, (uint64_t)tok * v_t * 4};
+  l4d_stash* st = nullptr;
+  if ((rc = stash_reserve_sized(A, x, kHeadStash, L4D_HEAD_COUNT, bytes, -1, &st))) return rc;
+  auto body = [&]() -> int {
+    int r;
+    HIP_TRY(hipMemcpyAsync(sptr<void>(st, L4D_HEAD_X), x_in, sp, hipMemcpyDeviceToDevice, s));
+    if ((r = launch("rmsnorm_fwd", s, [&] {
+           return rmsnorm_fwd(static_cast<const uint16_t*>(x_in), static_cast<const uint16_t*>(w_norm),
+                              sptr(st, L4D_HEAD_XN), x.b * x.s_sp, (int32_t)x.h, x.eps, s);
+         })))
+      return r;
+    EpiParams e{};
+    e.kind = EpiKind::StoreF32;
+    e.c = sptr<float>(st, L4D_HEAD_PROBS);
+    e.ldc = v_t;
+    if ((r = run_gemm("gemm_head_logits", s, tok, v_t, x.h, op(gathered(sptr(st, L4D_HEAD_XN), peer_xn, x), tok),
+                      Layout::KC, op(RowSrc::plain(w_lm, x.h), v_t), Layout::KC, e)))
+      return r;
+    return launch("xent_probs", s, [&] {
+      return xent_probs(sptr<float>(st, L4D_HEAD_PROBS), tok, (int32_t)v_t, v0, targets, peer_lse, peer_z, loss, s);
+    });
+  };
+  if ((rc = body())) {
+    l4d_stash_release(A, st);
+    return rc;
+  }
+  *stash_out = st;
+  return L4D_OK;
+}
+
+extern "C" int lm_head_bwd(const l4d_model* m, const l4d_parallel* p, const void* w_norm, const void* w_lm,
+                           const int64_t* targets, const void* peer_xn, const void* peer_dxn, void* dxn_send,
+                           float grad_scale, l4d_stash* st, void* dx, float* d_w_norm, float* d_w_lm, l4d_arena* A,
+                           void* stream_ptr) {
+  Shard x;
+  int rc = make_shard(m, p, &x);
+  if (rc) return rc;
+  int64_t v_t, v0;
+  if ((rc = vocab_shard(m, x, &v_t, &v0))) return rc;
+  if ((rc = check_ends_stash(A, st, kHeadStash, x))) return rc;
+  if (!w_norm || !w_lm || !targets || !dx || !d_w_norm || !d_w_lm)
+    return fail(L4D_EINVAL, "w_norm, w_lm, targets, dx, d_w_norm and d_w_lm are required");
+  if (x.t > 1 && !peer_xn) return fail(L4D_EINVAL, "tp > 1 needs peer_xn");
+  hipStream_t s = static_cast<hipStream_t>(stream_ptr);
+  const int64_t tok = x.b * x.s_c, rows_sp = x.b * x.s_sp;
+  const int32_t npart = rmsnorm_bwd_partials(rows_sp);
+  Carver cv;
+  const uint64_t o_dl = cv.take((uint64_t)tok * v_t * 2), o_dxn = cv.take((uint64_t)rows_sp * x.h * 2);
+  const uint64_t o_part = cv.take((uint64_t)npart * x.h * 4);
+  const uint64_t o_send = (x.t > 1 && !dxn_send) ? cv.take((uint64_t)x.b * (x.t - 1) * x.s_sp * x.h * 2) : 0;
+  Workspace ws;
+  if ((rc = take_ws(A, cv.used, ws))) return rc;
+  uint8_t* wsb = reinterpret_cast<uint8_t*>(A->base + ws.off);
+  uint16_t* dl = reinterpret_cast<uint16_t*>(wsb + o_dl);
+  uint16_t* dxn = reinterpret_cast<uint16_t*>(wsb + o_dxn);
+  float* partial = reinterpret_cast<float*>(wsb + o_part);
+  void* send = x.t > 1 ? (dxn_send ? dxn_send : (void*)(wsb + o_send)) : nullptr;
+  if ((rc = launch("xent_grad", s, [&] {
+         return xent_grad(sptr<const float>(st, L4D_HEAD_PROBS), tok, (int32_t)v_t, v0, targets, grad_scale, dl, s);
+       })))
+    return rc;
+  // d(xn) over the gathered rows: own rows + the peers' partials, the peers' rows sent
+  if ((rc = run_gemm("gemm_head_dx", s, tok, x.h, v_t, op(RowSrc::plain(dl, v_t), tok), Layout::KC,
+                     op(RowSrc::plain(w_lm, x.h), x.h), Layout::MN, epi_residual(x, dxn, nullptr, peer_dxn, send))))
+    return rc;
+  if ((rc = launch("rmsnorm_bwd", s, [&] {
+         return rmsnorm_bwd(sptr(st, L4D_HEAD_X), static_cast<const uint16_t*>(w_norm), dxn, nullptr,
+                            static_cast<uint16_t*>(dx), partial, npart, rows_sp, (int32_t)x.h, x.eps, s);
+       })))
+    return rc;
+  if ((rc = launch("reduce_gain", s, [&] { return reduce_rows_add(partial, npart, (int32_t)x.h, d_w_norm, s); })))
+    return rc;
+  if ((rc = run_gemm("gemm_head_dw", s, v_t, x.h, tok, op(RowSrc::plain(dl, v_t), v_t), Layout::MN,
+                     op(gathered(sptr(st, L4D_HEAD_XN), peer_xn, x), x.h), Layout::MN, epi_acc(d_w_lm, x.h))))
+    return rc;
+  return l4d_stash_release(A, st);
 }
 
 // ============================================================== optimizer

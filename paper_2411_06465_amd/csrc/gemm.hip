@@ -279,6 +279,18 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn,
       if (n_lo + PAIR < p.N) *reinterpret_cast<u32x4*>(c + n_lo + PAIR) = pack8(hi);
       break;
     }
+    case EpiKind::StoreF32: {
+      float* c = static_cast<float*>(e.c) + m * e.ldc;
+      if (n_lo < p.N) {
+        *reinterpret_cast<float4*>(c + n_lo) = make_float4(lo[0], lo[1], lo[2], lo[3]);
+        *reinterpret_cast<float4*>(c + n_lo + 4) = make_float4(lo[4], lo[5], lo[6], lo[7]);
+      }
+      if (n_lo + PAIR < p.N) {
+        *reinterpret_cast<float4*>(c + n_lo + PAIR) = make_float4(hi[0], hi[1], hi[2], hi[3]);
+        *reinterpret_cast<float4*>(c + n_lo + PAIR + 4) = make_float4(hi[4], hi[5], hi[6], hi[7]);
+      }
+      break;
+    }
     case EpiKind::AccF32:     // handled in registers (acc_load_f32 / acc_store_f32)
       break;
     case EpiKind::QkvRope: {
@@ -982,6 +994,7 @@ hipError_t gemm_variant(const GemmParams& p, Layout la, Layout lb, hipStream_t s
     if (k == E::ResidualSP) return launch<L::KC, L::KC, E::ResidualSP, 128>(p, stream, variant);
     if (k == E::SwiGLUFwd) return launch<L::KC, L::KC, E::SwiGLUFwd, 128>(p, stream, variant);
     if (k == E::StoreBF16) return launch<L::KC, L::KC, E::StoreBF16, 128>(p, stream, variant);
+    if (k == E::StoreF32) return launch<L::KC, L::KC, E::StoreF32, 128>(p, stream, variant);
   } else if (la == L::KC && lb == L::MN) {
     if (k == E::SwiGLUBwd) return launch<L::KC, L::MN, E::SwiGLUBwd, 128>(p, stream, variant);
     if (k == E::ResidualSP) return launch<L::KC, L::MN, E::ResidualSP, 128>(p, stream, variant);

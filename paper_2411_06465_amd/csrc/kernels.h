@@ -61,6 +61,7 @@ enum class Layout { KC, MN };
 
 enum class EpiKind {
   StoreBF16,    // C (bf16) = acc, row-major with ldc
+  StoreF32,     // C (f32) = acc, row-major with ldc
   AccF32,       // C (f32) += acc
   QkvRope,      // split [Q|K|V] columns, RoPE on Q and K, bf16
   ResidualSP,   // own rows: bf16(acc + resid + receipt); peer rows: bf16(acc) -> send buffer
@@ -176,6 +177,26 @@ hipError_t attn_bwd(const AttnParams& p, int part, hipStream_t stream);
 hipError_t xent_rows(const uint16_t* logits, int64_t n, int32_t v_t, int64_t v0,
                      const int64_t* targets, const float* peer_lse, const float* peer_z,
                      float grad_scale, float* loss, uint16_t* dlogits, hipStream_t stream);
+
+// FP32 logits [n][v_t] -> loss [n], and the rows overwritten in place with the
+// softmax over the whole vocabulary (LSE combined with peer_lse when given).
+hipError_t xent_probs(float* logits, int64_t n, int32_t v_t, int64_t v0, const int64_t* targets,
+                      const float* peer_lse, const float* peer_z, float* loss, hipStream_t stream);
+// dlogits (bf16 [n][v_t]) = (softmax - onehot(target)) * grad_scale.
+hipError_t xent_grad(const float* probs, int64_t n, int32_t v_t, int64_t v0, const int64_t* targets,
+                     float grad_scale, uint16_t* dlogits, hipStream_t stream);
+
+// ---------------------------------------------------------------- embedding
+
+// Gathered row m (0 <= m < rows = b*s_c) of the vocabulary-parallel lookup:
+// w[ids[m] - v0] if in [0, v_t) else 0; own SP rows -> own (+ receipt), the
+// peers' rows -> send (row mapping as RowSrc).
+hipError_t embed_fwd(const int64_t* ids, const uint16_t* w, int64_t v0, int32_t v_t, int32_t h, int64_t rows,
+                     int32_t s_c, int32_t s_sp, int32_t r, int32_t t, const uint16_t* receipt, uint16_t* own,
+                     uint16_t* send, hipStream_t stream);
+// dw[ids[m] - v0] += dy.row(m) for the ids in range (fp32 atomics).
+hipError_t embed_bwd(const int64_t* ids, RowSrc dy, int64_t v0, int32_t v_t, int32_t h, int64_t rows, float* dw,
+                     hipStream_t stream);
 
 // ---------------------------------------------------------------- optimizer
 

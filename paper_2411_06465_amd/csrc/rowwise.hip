@@ -1,5 +1,7 @@
 // Memory-bound row kernels: RMSNorm forward/backward, the gain-gradient
-// reduction, the RoPE angle table and the vocabulary-parallel cross-entropy.
+// reduction, the RoPE angle table, the vocabulary-parallel cross-entropy (bf16
+// logits, or FP32 logits kept as the softmax) and the vocabulary-parallel
+// embedding lookup and its gradient.
 // One wave (64 lanes) owns one row; every global access is a 16-byte vector.
 #include <math.h>
 
@@ -292,6 +294,146 @@ __global__ void __launch_bounds__(256) xent_rows_kernel(
   }
 }
 
+
+// FP32 logits [n][v_t] (v_t % 4 == 0), one 256-thread block per row: the loss,
+// and the row overwritten with the softmax exp(z - LSE) over the whole
+// vocabulary (LSE combined with the other shards' log-sum-exp).
+__global__ void __launch_bounds__(256) xent_probs_kernel(
+    float* __restrict__ lp, int32_t v_t, int64_t v0, const int64_t* __restrict__ targets,
+    const float* __restrict__ peer_lse, const float* __restrict__ peer_z, float* __restrict__ loss) {
+  __shared__ float red[4];
+  __shared__ float bcast;
+  const int64_t row = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float4* r4 = reinterpret_cast<float4*>(lp + row * v_t);
+  const int nch = v_t / 4;
+  float mx = -INFINITY;
+  for (int c = threadIdx.x; c < nch; c += 256) {
+    const float4 f = r4[c];
+    mx = fmaxf(mx, fmaxf(fmaxf(f.x, f.y), fmaxf(f.z, f.w)));
+  }
+  mx = wave_max(mx);
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  float se = 0.f;
+  for (int c = threadIdx.x; c < nch; c += 256) {
+    const float4 f = r4[c];
+    se += __expf(f.x - mx) + __expf(f.y - mx) + __expf(f.z - mx) + __expf(f.w - mx);
+  }
+  se = wave_sum(se);
+  if (lane == 0) red[wave] = se;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float lse = mx + logf(red[0] + red[1] + red[2] + red[3]);
+    if (peer_lse) {
+      const float p = peer_lse[row];
+      const float hi = fmaxf(lse, p), lo = fminf(lse, p);
+      lse = hi + log1pf(__expf(lo - hi));
+    }
+    const int64_t tgt = targets[row] - v0;
+    float z;
+    if (tgt >= 0 && tgt < v_t) z = lp[row * v_t + tgt];
+    else z = peer_z ? peer_z[row] : 0.f;
+    loss[row] = lse - z;
+    bcast = lse;
+  }
+  __syncthreads();
+  const float lse = bcast;
+  for (int c = threadIdx.x; c < nch; c += 256) {
+    const float4 f = r4[c];
+    r4[c] = make_float4(__expf(f.x - lse), __expf(f.y - lse), __expf(f.z - lse), __expf(f.w - lse));
+  }
+}
+
+// dlogits = (softmax - onehot(target)) * grad_scale as bf16, 8 elements per
+// thread over the flattened [n][v_t] (v_t % 8 == 0).
+__global__ void __launch_bounds__(256) xent_grad_kernel(const float* __restrict__ probs, int64_t n8, int32_t v8,
+                                                       int64_t v0, const int64_t* __restrict__ targets,
+                                                       float grad_scale, uint16_t* __restrict__ dl) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n8) return;
+  const int64_t row = i / v8;
+  const int32_t col0 = static_cast<int32_t>(i - row * v8) * 8;
+  const int64_t tgt = targets[row] - v0 - col0;
+  const float4* p4 = reinterpret_cast<const float4*>(probs) + 2 * i;
+  const float4 a = p4[0], b = p4[1];
+  float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = (j == tgt ? f[j] - 1.0f : f[j]) * grad_scale;
+  reinterpret_cast<u32x4*>(dl)[i] = pack8(f);
+}
+
+// ------------------------------------------------------------------ embedding
+// Rows of the gathered [b][s_c] token view are split between this rank's own
+// sequence-parallel rows and the peers' rows as in the layer (SpRows below).
+
+struct SpRows {
+  int32_t s_c, s_sp, r, t;
+  // logical row m -> (own row index) or (peer row index) | 0x80000000
+  __device__ uint32_t map(int64_t m64) const {
+    const int32_t m = static_cast<int32_t>(m64);
+    if (t == 1) return static_cast<uint32_t>(m);
+    const int32_t bi = m / s_c, i = m - bi * s_c, lo = r * s_sp;
+    if (i >= lo && i < lo + s_sp) return static_cast<uint32_t>(bi * s_sp + (i - lo));
+    return static_cast<uint32_t>(bi * (t - 1) * s_sp + (i < lo ? i : i - s_sp)) | 0x80000000u;
+  }
+};
+
+// One wave per gathered row: the table row when the id is in [v0, v0 + v_t),
+// zeros otherwise.  Own rows: bf16(partial + receipt); peer rows: the partial.
+__global__ void __launch_bounds__(256) embed_fwd_kernel(const int64_t* __restrict__ ids,
+                                                       const uint16_t* __restrict__ w, int64_t v0, int32_t v_t,
+                                                       int32_t h, int64_t rows, SpRows sp,
+                                                       const uint16_t* __restrict__ receipt,
+                                                       uint16_t* __restrict__ own, uint16_t* __restrict__ send) {
+  const int lane = threadIdx.x & 63;
+  const int64_t m = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (m >= rows) return;
+  const int64_t j = ids[m] - v0;
+  const bool hit = j >= 0 && j < v_t;
+  const uint32_t o = sp.map(m);
+  const bool mine = !(o & 0x80000000u);
+  const int64_t orow = o & 0x7fffffffu;
+  u32x4* dst = reinterpret_cast<u32x4*>((mine ? own : send) + orow * h);
+  const u32x4* src = reinterpret_cast<const u32x4*>(w + (hit ? j : 0) * h);
+  const u32x4* rc = (mine && receipt) ? reinterpret_cast<const u32x4*>(receipt + orow * h) : nullptr;
+  for (int c = lane; c < h / 8; c += 64) {
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    const u32x4 v = hit ? src[c] : z;
+    if (rc) {
+      float a[8], b[8];
+      unpack8(v, a);
+      unpack8(rc[c], b);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a[e] += b[e];
+      dst[c] = pack8(a);
+    } else {
+      dst[c] = v;
+    }
+  }
+}
+
+// One wave per gathered row whose id is in range: dW[id - v0] += dY[row]
+// (fp32 atomic adds: rows that share an id add in no fixed order).
+__global__ void __launch_bounds__(256) embed_bwd_kernel(const int64_t* __restrict__ ids, RowSrc dy, int64_t v0,
+                                                       int32_t v_t, int32_t h, int64_t rows, float* __restrict__ dw) {
+  const int lane = threadIdx.x & 63;
+  const int64_t m = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (m >= rows) return;
+  const int64_t j = ids[m] - v0;
+  if (j < 0 || j >= v_t) return;
+  const u32x4* src = reinterpret_cast<const u32x4*>(dy.row(m));
+  float* d = dw + j * h;
+  for (int c = lane; c < h / 8; c += 64) {
+    float f[8];
+    unpack8(src[c], f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) unsafeAtomicAdd(d + c * 8 + e, f[e]);
+  }
+}
+
 }  // namespace
 
 hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* gain, uint16_t* y, int64_t rows, int32_t h,
@@ -342,6 +484,40 @@ hipError_t xent_rows(const uint16_t* logits, int64_t n, int32_t v_t, int64_t v0,
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(xent_rows_kernel, dim3(static_cast<unsigned>(n)), dim3(256), 0, stream, logits, v_t, v0,
                      targets, peer_lse, peer_z, grad_scale, loss, dlogits);
+  return hipGetLastError();
+}
+
+hipError_t xent_probs(float* logits, int64_t n, int32_t v_t, int64_t v0, const int64_t* targets,
+                      const float* peer_lse, const float* peer_z, float* loss, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(xent_probs_kernel, dim3(static_cast<unsigned>(n)), dim3(256), 0, stream, logits, v_t, v0,
+                     targets, peer_lse, peer_z, loss);
+  return hipGetLastError();
+}
+
+hipError_t xent_grad(const float* probs, int64_t n, int32_t v_t, int64_t v0, const int64_t* targets,
+                     float grad_scale, uint16_t* dlogits, hipStream_t stream) {
+  const int64_t n8 = n * (v_t / 8);
+  if (n8 <= 0) return hipSuccess;
+  hipLaunchKernelGGL(xent_grad_kernel, dim3(static_cast<unsigned>((n8 + 255) / 256)), dim3(256), 0, stream, probs,
+                     n8, v_t / 8, v0, targets, grad_scale, dlogits);
+  return hipGetLastError();
+}
+
+hipError_t embed_fwd(const int64_t* ids, const uint16_t* w, int64_t v0, int32_t v_t, int32_t h, int64_t rows,
+                     int32_t s_c, int32_t s_sp, int32_t r, int32_t t, const uint16_t* receipt, uint16_t* own,
+                     uint16_t* send, hipStream_t stream) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_fwd_kernel, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, ids, w,
+                     v0, v_t, h, rows, SpRows{s_c, s_sp, r, t}, receipt, own, send);
+  return hipGetLastError();
+}
+
+hipError_t embed_bwd(const int64_t* ids, RowSrc dy, int64_t v0, int32_t v_t, int32_t h, int64_t rows, float* dw,
+                     hipStream_t stream) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_bwd_kernel, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, ids, dy,
+                     v0, v_t, h, rows, dw);
   return hipGetLastError();
 }
 

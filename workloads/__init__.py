@@ -255,3 +255,91 @@ def adam_inputs_device(name, n, device="cuda"):
 # rank (1,201,045,504: the LM-head shard and 10 layers), divided over the
 # d c = 4 ranks that share the optimizer states.
 ADAM_70B_SHARD = AdamWorkload("llama3-70b-tp8pp8dp4-optimizer-shard", 300_261_376)
+
+
+# ---------------------------------------------------------------- the ends of the model
+
+@dataclass(frozen=True)
+class EndsWorkload:
+    """Embedding and LM-head block of one (TP, CP) rank: model dims, sequence,
+    micro-batch and the layout (TP/CP sizes and ranks)."""
+    name: str
+    hidden: int
+    n_heads: int
+    n_kv_heads: int
+    ffn: int
+    vocab: int
+    seq: int
+    micro_batch: int = 1
+    tp: int = 1
+    cp: int = 1
+    tp_rank: int = 0
+    cp_rank: int = 0
+    rms_eps: float = 1e-5
+
+    @property
+    def s_c(self):
+        return self.seq // self.cp
+
+    @property
+    def s_sp(self):
+        return self.s_c // self.tp
+
+    @property
+    def v_t(self):
+        return self.vocab // self.tp
+
+    @property
+    def tokens(self):
+        return self.micro_batch * self.s_c
+
+    def model(self):
+        return dict(hidden=self.hidden, n_heads=self.n_heads, n_kv_heads=self.n_kv_heads, ffn=self.ffn,
+                    n_layers=1, vocab=self.vocab, rms_eps=self.rms_eps)
+
+    def parallel(self):
+        return dict(seq=self.seq, micro_batch=self.micro_batch, tp=self.tp, cp=self.cp, pp=1, dp=1,
+                    tp_rank=self.tp_rank, cp_rank=self.cp_rank)
+
+
+def ends_inputs(w: EndsWorkload):
+    """Embedding: table shard N(0, 0.02) bf16; token ids Zipf-distributed over a
+    seeded permutation of the vocabulary (natural text repeats a few ids
+    often); the peers' partial rows for the own rows (the table row when
+    another rank holds the id, else zero); output gradients N(0, 1).
+    LM head: x N(0, 1), final-norm gain 1 + N(0, 0.02), head shard N(0, 0.02),
+    targets uniform over the vocabulary, the peers' normed rows N(0, 1), peer
+    log-sum-exp N(ln((t-1) v_t), 0.1), peer target logits N(0, 1.28), the
+    peers' partial d(xn) N(0, 0.02 / tokens)."""
+    n, b, h, t = w.name, w.micro_batch, w.hidden, w.tp
+    own, peer = (b, w.s_sp, h), (b, (t - 1) * w.s_sp, h)
+    perm = _rng(n, "perm").permutation(w.vocab)
+    ids = perm[(_rng(n, "zipf").zipf(1.3, size=(b, w.s_c)) - 1) % w.vocab].astype(np.int64)
+    v0 = w.tp_rank * w.v_t
+    own_ids = ids[:, w.tp_rank * w.s_sp:(w.tp_rank + 1) * w.s_sp]
+    elsewhere = (own_ids < v0) | (own_ids >= v0 + w.v_t)
+    receipt = _rng(n, "receipt").standard_normal(own, dtype=np.float32) * np.float32(0.02)
+    receipt *= elsewhere[..., None]
+    out = dict(
+        w_emb=bf16_normal((w.v_t, h), 0.02, 0.0, n, "w_emb"), ids=ids, emb_receipt=f32_to_bf16_bits(receipt),
+        dx_emb=bf16_normal(own, 1.0, 0.0, n, "dx_emb"),
+        x=bf16_normal(own, 1.0, 0.0, n, "x"), w_norm=bf16_normal((h,), 0.02, 1.0, n, "w_norm"),
+        w_lm=bf16_normal((w.v_t, h), 0.02, 0.0, n, "w_lm"),
+        targets=_rng(n, "targets").integers(0, w.vocab, size=w.tokens, dtype=np.int64),
+    )
+    if t > 1:
+        out["peer_dx_emb"] = bf16_normal(peer, 1.0, 0.0, n, "peer_dx_emb")
+        out["peer_xn"] = bf16_normal(peer, 1.0, 0.0, n, "peer_xn")
+        out["peer_lse"] = (_rng(n, "peer_lse").standard_normal(w.tokens) * 0.1
+                           + np.log((t - 1) * w.v_t)).astype(np.float32)
+        out["peer_target_logit"] = (_rng(n, "peer_z").standard_normal(w.tokens) * 1.28).astype(np.float32)
+        out["peer_dxn"] = bf16_normal(own, 0.02 / w.tokens, 0.0, n, "peer_dxn")
+    return out
+
+
+ENDS_TINY = EndsWorkload("ends-tiny", 256, 4, 2, 688, 1024, 128)
+ENDS_TP2CP2_RAGGED = EndsWorkload("ends-tp2cp2-ragged", 512, 4, 2, 1376, 2000, 400, micro_batch=2, tp=2, cp=2,
+                                  tp_rank=1, cp_rank=1)
+ENDS_MID = EndsWorkload("ends-mid-tp2", 1024, 8, 8, 2816, 8192, 1024, tp=2, tp_rank=0)
+# The Llama-3-8B head at TP4 (8192 tokens, vocabulary shard 32064 of 128256).
+ENDS_LLAMA3_8B_TP4 = EndsWorkload("ends-llama3-8b-tp4", 4096, 32, 8, 14336, 128256, 8192, tp=4, tp_rank=1)
