@@ -29,6 +29,9 @@
 
 #include <type_traits>
 
+#include <algorithm>
+#include <vector>
+
 #include "kernels.h"
 
 namespace l4d {
@@ -523,7 +526,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int group = p.a_t / p.k_t;
   const int hpb = group / p.n_split;
   const int nyz = p.k_t * p.n_split * p.b;
-  const int kb = static_cast<int>(blockIdx.x) / nyz, yz = static_cast<int>(blockIdx.x) % nyz;
+  const int kb_raw = static_cast<int>(blockIdx.x) / nyz, yz = static_cast<int>(blockIdx.x) % nyz;
+  const int kb = p.n_order ? p.kb_order[kb_raw] : kb_raw;
   const int hk = yz % (p.k_t * p.n_split) / p.n_split, split = yz % p.n_split;
   const int bi = yz / (p.k_t * p.n_split);
   int seg, k0;
@@ -905,6 +909,38 @@ hipError_t fwd_impl(const AttnParams& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// Host copy of the query-tile walk of the dK/dV kernel: the number of 64-query
+// tiles a 128-key block starting at global position kpos0 visits per head.
+int dkdv_tiles(const AttnParams& p, int kpos0) {
+  const int n_qt = (p.n_q + QT - 1) / QT;
+  int n = 0;
+  for (int qt = 0; qt < n_qt; ++qt) {
+    const int last = std::min(qt * QT + QT - 1, p.n_q - 1);
+    const bool second = last >= p.qmap.chunk_len;
+    const int pos = (second ? p.qmap.chunk_id[1] : p.qmap.chunk_id[0]) * p.qmap.chunk_len +
+                    (second ? last - p.qmap.chunk_len : last);
+    if (pos >= kpos0) ++n;
+  }
+  return n;
+}
+
+// Dispatch order of the dK/dV key blocks: most query tiles first (stable), so
+// that with context parallelism the long blocks of every key segment start
+// before the short ones instead of segment by segment.
+void dkdv_order(AttnParams& p) {
+  const int nb = count_blocks(p, 128);
+  p.n_order = 0;
+  if (nb > kMaxKeyBlocks) return;
+  std::vector<std::pair<int, int>> w;
+  w.reserve(nb);
+  int kb = 0;
+  for (int s = 0; s < p.n_seg; ++s)
+    for (int k0 = 0; k0 < p.seg[s].n; k0 += 128, ++kb) w.push_back({-dkdv_tiles(p, p.seg[s].pos0 + k0), kb});
+  std::stable_sort(w.begin(), w.end(), [](const auto& a, const auto& b) { return a.first < b.first; });
+  for (int i = 0; i < nb; ++i) p.kb_order[i] = static_cast<uint16_t>(w[i].second);
+  p.n_order = nb;
+}
+
 template <int D>
 hipError_t bwd_impl(const AttnParams& p, int part, hipStream_t stream) {
   if (part == 0) {
@@ -912,7 +948,9 @@ hipError_t bwd_impl(const AttnParams& p, int part, hipStream_t stream) {
     hipLaunchKernelGGL(attn_delta_kernel<D>, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, p);
   } else if (part == 1) {
     const unsigned blocks = static_cast<unsigned>(count_blocks(p, 128)) * p.k_t * p.n_split * p.b;
-    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(blocks), dim3(512), 0, stream, p);
+    AttnParams q = p;
+    dkdv_order(q);
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(blocks), dim3(512), 0, stream, q);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.n_split == 1) return e;
     hipLaunchKernelGGL(attn_dkv_reduce_kernel<D>, dim3(p.total_keys, p.k_t, p.b), dim3(64), 0, stream, p);

@@ -164,7 +164,13 @@ struct AttnParams {
   int32_t seg_key0[kMaxSeg];   // index of each segment's first key among them
   float* dkv_partial;
   int64_t partial_half;
+  // dK/dV: the 128-key blocks in the order the grid dispatches them (heaviest
+  // first; filled by attn_bwd when there are at most kMaxKeyBlocks, else n_order = 0
+  // and blocks go in key order)
+  int32_t n_order;
+  uint16_t kb_order[512];
 };
+constexpr int kMaxKeyBlocks = 512;
 
 // Number of query-head slices the dK/dV pass uses for this shape (1 = none).
 int attn_bwd_splits(const AttnParams& p);
