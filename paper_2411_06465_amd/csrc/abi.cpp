@@ -488,8 +488,12 @@ struct FwdWs {
   uint64_t rope, o_send, ffn_send, total;
 };
 struct BwdWs {
-  uint64_t rope, dgu, dxn2, dh1, dctx, delta, dqkv, dxn1, partial, dxn2_send, dxn1_send, dkv, total;
+  uint64_t rope, dgu, dxn2, dh1, dctx, delta, dqkv, dxn1, partial, dxn2_send, dxn1_send, dkv, dwpart, total;
 };
+
+uint64_t split_ws_bytes(int64_t M, int64_t N, int64_t K) {
+  return (uint64_t)(gemm_ksplits(M, N, K) - 1) * M * N * 4;
+}
 
 FwdWs plan_fwd(const Shard& x, const l4d_peer_outputs* sends) {
   Carver cv;
@@ -521,6 +525,11 @@ BwdWs plan_bwd(const Shard& x, const l4d_peer_outputs* sends) {
   // fp32 dK/dV partials when the query heads of a kv-head are split (at most a/k slices)
   const int64_t group = x.a / x.k;
   w.dkv = group > 1 ? cv.take(2 * (uint64_t)group * x.b * x.s * x.k_t * x.d * 4) : 0;
+  // fp32 partials of the weight-gradient GEMMs that split their K (token) range
+  const int64_t tk = (int64_t)tok;
+  const uint64_t dwp = std::max({split_ws_bytes(x.h, x.f_t, tk), split_ws_bytes(2 * x.f_t, x.h, tk),
+                                 split_ws_bytes(x.h, x.a_t * x.d, tk), split_ws_bytes(qkv_cols(x), x.h, tk)});
+  w.dwpart = dwp ? cv.take(dwp) : 0;
   w.total = cv.used;
   return w;
 }
@@ -594,8 +603,10 @@ inline EpiParams epi_store(void* c, int64_t ldc) {
   return e;
 }
 
+// split_ws: room for the fp32 partials of a split K range (AccF32 only; NULL =
+// never split); split_ws_bytes(M, N, K) bytes are needed.
 int run_gemm(const char* name, hipStream_t s, int64_t M, int64_t N, int64_t K, Operand A, Layout la, Operand B,
-             Layout lb, EpiParams e) {
+             Layout lb, EpiParams e, float* split_ws = nullptr) {
   GemmParams p{};
   p.M = (int32_t)M;
   p.N = (int32_t)N;
@@ -603,7 +614,15 @@ int run_gemm(const char* name, hipStream_t s, int64_t M, int64_t N, int64_t K, O
   p.A = A;
   p.B = B;
   p.epi = e;
-  return launch(name, s, [&] { return gemm(p, la, lb, s); });
+  if (e.kind == EpiKind::AccF32 && split_ws) {
+    p.k_splits = gemm_ksplits(M, N, K);
+    p.partial = split_ws;
+  }
+  int rc = launch(name, s, [&] { return gemm(p, la, lb, s); });
+  if (rc || p.k_splits <= 1) return rc;
+  return launch("gemm_splitk_reduce", s, [&] {
+    return gemm_split_reduce(static_cast<float*>(e.c), e.ldc, split_ws, M, N, p.k_splits, s);
+  });
 }
 
 // Key runs of the attention: local chunks (stash K/V) then remote runs.
@@ -825,6 +844,7 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
   uint16_t *dqkv = W(plan.dqkv), *dxn1 = W(plan.dxn1);
   float* delta = reinterpret_cast<float*>(wsb + plan.delta);
   float* partial = reinterpret_cast<float*>(wsb + plan.partial);
+  float* dwpart = plan.dwpart ? reinterpret_cast<float*>(wsb + plan.dwpart) : nullptr;
   const l4d_peer_inputs none{};
   const l4d_peer_inputs& pi = peers ? *peers : none;
   void* dxn2_send = (sends && sends->dxn2_partial) ? sends->dxn2_partial : (void*)W(plan.dxn2_send);
@@ -850,7 +870,7 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
       return r;
     // dW_down += dy_full^T prod
     if ((r = run_gemm("gemm_down_dw", s, x.h, x.f_t, tok, op(dy_full, x.h), Layout::MN,
-                      op(RowSrc::plain(sptr(st, L4D_STASH_PROD), x.f_t), x.f_t), Layout::MN, epi_acc(dw->down, x.f_t))))
+                      op(RowSrc::plain(sptr(st, L4D_STASH_PROD), x.f_t), x.f_t), Layout::MN, epi_acc(dw->down, x.f_t), dwpart)))
       return r;
     // d(xn2) = dGU W_gu (own rows + receipt; peers' rows sent)
     if ((r = run_gemm("gemm_gate_up_dx", s, tok, x.h, 2 * x.f_t, op(RowSrc::plain(dgu, 2 * x.f_t), tok), Layout::KC,
@@ -859,7 +879,7 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
       return r;
     const RowSrc xn2_full = gathered(sptr(st, L4D_STASH_XN2), pi.sp_peer_xn2, x);
     if ((r = run_gemm("gemm_gate_up_dw", s, 2 * x.f_t, x.h, tok, op(RowSrc::plain(dgu, 2 * x.f_t), 2 * x.f_t),
-                      Layout::MN, op(xn2_full, x.h), Layout::MN, epi_acc(dw->gate_up, x.h))))
+                      Layout::MN, op(xn2_full, x.h), Layout::MN, epi_acc(dw->gate_up, x.h), dwpart)))
       return r;
     // norm-2 backward + residual
     if ((r = launch("rmsnorm_bwd", s, [&] {
@@ -875,7 +895,7 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
                       Layout::MN, epi_store(dctx, nq))))
       return r;
     if ((r = run_gemm("gemm_o_dw", s, x.h, nq, tok, op(dh1_full, x.h), Layout::MN,
-                      op(RowSrc::plain(sptr(st, L4D_STASH_CTX), nq), nq), Layout::MN, epi_acc(dw->o, nq))))
+                      op(RowSrc::plain(sptr(st, L4D_STASH_CTX), nq), nq), Layout::MN, epi_acc(dw->o, nq), dwpart)))
       return r;
     // attention backward -> dQKV (inverse RoPE applied), remote dK/dV
     AttnParams ap = attn_params(x);
@@ -911,7 +931,7 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
       return r;
     const RowSrc xn1_full = gathered(sptr(st, L4D_STASH_XN1), pi.sp_peer_xn1, x);
     if ((r = run_gemm("gemm_qkv_dw", s, qc, x.h, tok, op(RowSrc::plain(dqkv, qc), qc), Layout::MN, op(xn1_full, x.h),
-                      Layout::MN, epi_acc(dw->qkv, x.h))))
+                      Layout::MN, epi_acc(dw->qkv, x.h), dwpart)))
       return r;
     // norm-1 backward + residual
     if ((r = launch("rmsnorm_bwd", s, [&] {

@@ -488,9 +488,8 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, f32x16 (&acc)[4]
 // the 32 lanes of a half-wave cover 32 consecutive columns (128 bytes) of one
 // row, so both are whole-line accesses without staging.
 template <int NS>
-__device__ __forceinline__ void acc_load_f32(f32x16 (&acc)[4][NS], const GemmParams& p, int64_t row0, int tn,
-                                             const int* ncol, int lane) {
-  const int64_t ldc = p.epi.ldc;
+__device__ __forceinline__ void acc_load_f32(f32x16 (&acc)[4][NS], const GemmParams& p, const float* cbase,
+                                             int64_t ldc, int64_t row0, int tn, const int* ncol, int lane) {
   const int rl = 4 * (lane >> 5);
   int32_t off[NS];            // lane's element offset from its row block's first row
 #pragma unroll
@@ -501,7 +500,7 @@ __device__ __forceinline__ void acc_load_f32(f32x16 (&acc)[4][NS], const GemmPar
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int r = ms * 32 + 8 * (i >> 2) + (i & 3);
-      const float* row = static_cast<const float*>(p.epi.c) + (row0 + r) * ldc;   // uniform
+      const float* row = cbase + (row0 + r) * ldc;   // uniform
 #pragma unroll
       for (int ns = 0; ns < NS; ++ns) {
         if (full) {
@@ -515,9 +514,8 @@ __device__ __forceinline__ void acc_load_f32(f32x16 (&acc)[4][NS], const GemmPar
 }
 
 template <int NS>
-__device__ __forceinline__ void acc_store_f32(const f32x16 (&acc)[4][NS], const GemmParams& p, int64_t row0, int tn,
-                                              const int* ncol, int lane) {
-  const int64_t ldc = p.epi.ldc;
+__device__ __forceinline__ void acc_store_f32(const f32x16 (&acc)[4][NS], const GemmParams& p, float* cbase,
+                                              int64_t ldc, int64_t row0, int tn, const int* ncol, int lane) {
   const int rl = 4 * (lane >> 5);
   int32_t off[NS];
 #pragma unroll
@@ -528,7 +526,7 @@ __device__ __forceinline__ void acc_store_f32(const f32x16 (&acc)[4][NS], const 
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int r = ms * 32 + 8 * (i >> 2) + (i & 3);
-      float* row = static_cast<float*>(p.epi.c) + (row0 + r) * ldc;
+      float* row = cbase + (row0 + r) * ldc;
 #pragma unroll
       for (int ns = 0; ns < NS; ++ns) {
         const int n = tn * BN + ncol[ns] + (lane & 31);
@@ -583,7 +581,8 @@ __global__ void __launch_bounds__(512, 1) gemm_bk32(GemmParams p) {
 
   f32x16 acc[4][NS];
   if constexpr (KIND == EpiKind::AccF32) {
-    acc_load_f32<NS>(acc, p, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
+    acc_load_f32<NS>(acc, p, static_cast<float*>(p.epi.c), p.epi.ldc, static_cast<int64_t>(m0) + wm * 128, tn,
+                     ncol, lane);
   } else {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -659,7 +658,8 @@ __global__ void __launch_bounds__(512, 1) gemm_bk32(GemmParams p) {
   if (rest > 2) step(kt + 2, a2, b2, a1, b1);
   wait_vm<0>();      // no copy may land in the stages once they are staging space (or after the end)
   if constexpr (KIND == EpiKind::AccF32) {
-    acc_store_f32<NS>(acc, p, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
+    acc_store_f32<NS>(acc, p, static_cast<float*>(p.epi.c), p.epi.ldc, static_cast<int64_t>(m0) + wm * 128, tn,
+                      ncol, lane);
   } else {
     __syncthreads();   // every wave is done reading the stages before they become staging space
     uint8_t* mine = wave == 0 ? a0 : wave == 1 ? b0 : wave == 2 ? a1 : wave == 3 ? b1 : wave == 4 ? a2
@@ -911,7 +911,13 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   __shared__ __attribute__((aligned(16))) uint8_t a0[TILE2], b0[TILE2], a1[TILE2], b1[TILE2];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave: scalar code for wave-level decisions
-  const TileCoord tc = tile_of(p);
+  // AccF32 with a split K range: the grid is k_splits copies of the tile grid,
+  // part-major after the XCD remap, so an XCD's neighbouring tiles share a part.
+  const int parts = KIND == EpiKind::AccF32 && p.k_splits > 1 ? p.k_splits : 1;
+  const int pid_all = xcd_remap(blockIdx.x, gridDim.x);
+  const int tiles = static_cast<int>(gridDim.x) / parts;
+  const int part = pid_all / tiles;
+  const TileCoord tc = tile_coord(p, pid_all - part * tiles);
   const int tm = tc.tm, tn = tc.tn, m0 = tm * BM;
   const int wm = WAVES == 8 ? (wave >> 2) : (wave >> 1);
   const int wn = WAVES == 8 ? (wave & 3) : (wave & 1);
@@ -921,21 +927,28 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
     ncol[j] = lo_col<WAVES, PAIR>(wn, j);
     ncol[j + NS / 2] = ncol[j] + PAIR;
   }
+  const int n_st = p.K / BK2 / parts;          // stages per part (the host keeps it even)
+  float* cbase = nullptr;
+  int64_t ldc = 0;
+  if constexpr (KIND == EpiKind::AccF32) {
+    cbase = part == 0 ? static_cast<float*>(p.epi.c) : p.partial + static_cast<int64_t>(part - 1) * p.M * p.N;
+    ldc = part == 0 ? p.epi.ldc : p.N;
+  }
 
   f32x16 acc[4][NS];
-  if constexpr (KIND == EpiKind::AccF32) {
-    acc_load_f32<NS>(acc, p, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
+  if (KIND == EpiKind::AccF32 && part == 0) {
+    acc_load_f32<NS>(acc, p, cbase, ldc, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
   } else {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
   }
-  // K is a multiple of 2 * BK2 (the host picks this kernel only then).
-  mainloop64<LA, LB, WAVES, KIND == EpiKind::AccF32>(p, acc, tm, tn, 0, p.K / BK2, a0, b0, a1, b1, wave,
+  // K is a multiple of 2 * BK2 * parts (the host picks this kernel only then).
+  mainloop64<LA, LB, WAVES, KIND == EpiKind::AccF32>(p, acc, tm, tn, part * n_st, n_st, a0, b0, a1, b1, wave,
                                                              lane, wm, ncol);
   if constexpr (KIND == EpiKind::AccF32) {
-    acc_store_f32<NS>(acc, p, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
+    acc_store_f32<NS>(acc, p, cbase, ldc, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
   } else {
     __syncthreads();   // every wave is done reading the stages
     store_tile<KIND, PAIR, NS>(p, acc, stage_space<WAVES>(a0, b0, a1, b1, wave), static_cast<int64_t>(m0) + wm * 128,
@@ -958,10 +971,14 @@ template <Layout LA, Layout LB, EpiKind KIND, int PAIR>
 hipError_t launch(const GemmParams& p, hipStream_t stream, int variant) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = p.B.split_rows ? (p.B.split_rows + 127) / 128 : (p.N + BN - 1) / BN;
-  const dim3 grid(tiles_m * tiles_n);
+  const int parts = p.k_splits > 1 ? p.k_splits : 1;
+  if (parts > 1 && (KIND != EpiKind::AccF32 || p.K % (2 * BK2 * parts) != 0 || !p.partial))
+    return hipErrorInvalidValue;
+  const dim3 grid(tiles_m * tiles_n * parts);
   if (variant == 0) variant = gemm_variant_env();
   if (variant == 0) variant = 68;
   if (p.K % (2 * BK2) != 0) variant = 32;
+  if (parts > 1) variant = 68;
   if constexpr (LA == Layout::MN) {
     if (variant == 64) variant = 68;     // the 4-wave kernel needs stack space with two MN operands
   }
@@ -1003,6 +1020,58 @@ hipError_t gemm_variant(const GemmParams& p, Layout la, Layout lb, hipStream_t s
     if (k == E::AccF32) return launch<L::MN, L::MN, E::AccF32, 128>(p, stream, variant);
   }
   return hipErrorInvalidValue;     // a layout / epilogue pairing the layer never uses
+}
+
+namespace {
+// C += partial[0] + partial[1] + ..., four floats per thread (N % 4 == 0 and
+// ldc % 4 == 0 are required by the caller).
+__global__ void __launch_bounds__(256) split_reduce_kernel(float* __restrict__ c, int64_t ldc,
+                                                          const float* __restrict__ part, int64_t M, int64_t N,
+                                                          int32_t n_part) {
+  const int64_t n4 = N / 4;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= M * n4) return;
+  const int64_t m = i / n4, j = (i - m * n4) * 4;
+  float4* cp = reinterpret_cast<float4*>(c + m * ldc + j);
+  float4 v = *cp;
+  for (int s = 0; s < n_part; ++s) {
+    const float4 q = *reinterpret_cast<const float4*>(part + static_cast<int64_t>(s) * M * N + m * N + j);
+    v.x += q.x;
+    v.y += q.y;
+    v.z += q.z;
+    v.w += q.w;
+  }
+  *cp = v;
+}
+}  // namespace
+
+int gemm_ksplits(int64_t M, int64_t N, int64_t K) {
+  // Model: a wave of 256 tiles of full K takes T = 2*256*256*K / (1 PFLOP/s / 256 CUs);
+  // s parts take ceil(tiles*s / 256) waves of T/s, plus writing and reading the
+  // s - 1 fp32 partials at about 4 TB/s.  Pick the cheapest s of 1..4.
+  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  const double t_wave = 2.0 * BM * BN * static_cast<double>(K) / (1e15 / 256.0);
+  int best = 1;
+  double best_t = 1e30;
+  for (int s = 1; s <= 4; ++s) {
+    if (K % (2 * BK2 * s) != 0 || N % 4 != 0) continue;
+    const double waves = static_cast<double>((tiles * s + 255) / 256);
+    const double t = waves * t_wave / s + (s - 1) * 2.0 * 4.0 * static_cast<double>(M) * N / 4e12;
+    if (t < best_t * 0.97) {       // a split has to win by a margin
+      best_t = t;
+      best = s;
+    }
+  }
+  return best;
+}
+
+hipError_t gemm_split_reduce(float* c, int64_t ldc, const float* partial, int64_t M, int64_t N, int32_t splits,
+                             hipStream_t stream) {
+  if (splits <= 1 || M <= 0 || N <= 0) return hipSuccess;
+  const int64_t n = M * (N / 4);
+  hipLaunchKernelGGL(split_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, c, ldc,
+                     partial, M, N, splits - 1);
+  return hipGetLastError();
 }
 
 }  // namespace l4d

@@ -95,9 +95,21 @@ struct GemmParams {
   int32_t M, N, K;
   Operand A, B;
   EpiParams epi;
+  // AccF32 only: the K range is cut into k_splits equal parts (0 or 1 = none).
+  // Part 0 accumulates into C; part s > 0 stores its fp32 sum to
+  // partial + (s - 1) M N (row-major, ld N), which gemm_split_reduce then adds
+  // to C in order s = 1, 2, ...
+  int32_t k_splits;
+  float* partial;
 };
 
 hipError_t gemm(const GemmParams& p, Layout la, Layout lb, hipStream_t stream);
+// Parts the K range of an fp32-accumulate GEMM is cut into when one tile per
+// workgroup would leave much of the chip idle (1 = no split).
+int gemm_ksplits(int64_t M, int64_t N, int64_t K);
+// C[m][n] += sum over s of partial[s][m][n], s = 0 .. splits - 2, in that order.
+hipError_t gemm_split_reduce(float* c, int64_t ldc, const float* partial, int64_t M, int64_t N, int32_t splits,
+                             hipStream_t stream);
 
 // ---------------------------------------------------------------- row-wise kernels
 

@@ -27,6 +27,9 @@ CASES = {
     "d128-s384": W.LayerWorkload("d128-s384", 512, 4, 2, 1376, 384, rope_base=5e5),
     "gqa8-cp2-s320": W.LayerWorkload("gqa8-cp2", 1024, 8, 1, 512, 320, cp=2, cp_rank=0, n_gpus=2, rope_base=5e5),
     "mha-cp4-r2": W.LayerWorkload("mha-cp4", 512, 4, 4, 768, 512, cp=4, cp_rank=2, n_gpus=4, rope_base=1e4),
+    # 1024 tokens over few weight-gradient tiles: those GEMMs cut their token range in 4 parts
+    # (d128-s384: in 3), each part summed in fp32 and added to the accumulator in order
+    "d128-s1024-splitk": W.LayerWorkload("d128-s1024", 512, 4, 2, 1376, 1024, rope_base=5e5),
 }
 
 
@@ -61,8 +64,9 @@ def test_layer_matches_oracle(name):
     assert ok, "\n".join(rep)
 
 
-def test_layer_is_deterministic_and_accumulates_gradients():
-    w = CASES["tiny-cp2-r1"]
+@pytest.mark.parametrize("name", ["tiny-cp2-r1", "d128-s384"])
+def test_layer_is_deterministic_and_accumulates_gradients(name):
+    w = CASES[name]
     buf = Buffers(w)
     buf.run(keep_stash=False)
     y1, dx1 = buf.y.clone(), buf.dx.clone()
