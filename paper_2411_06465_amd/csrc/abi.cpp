@@ -491,8 +491,9 @@ struct BwdWs {
   uint64_t rope, dgu, dxn2, dh1, dctx, delta, dqkv, dxn1, partial, dxn2_send, dxn1_send, dkv, dwpart, total;
 };
 
-uint64_t split_ws_bytes(int64_t M, int64_t N, int64_t K) {
-  return (uint64_t)(gemm_ksplits(M, N, K) - 1) * M * N * 4;
+uint64_t split_ws_bytes(int64_t M, int64_t N, int64_t K, bool acc_f32 = true) {
+  const int s = gemm_ksplits(M, N, K, acc_f32);
+  return s <= 1 ? 0 : (uint64_t)(acc_f32 ? s - 1 : s) * M * N * 4;
 }
 
 FwdWs plan_fwd(const Shard& x, const l4d_peer_outputs* sends) {
@@ -528,7 +529,8 @@ BwdWs plan_bwd(const Shard& x, const l4d_peer_outputs* sends) {
   // fp32 partials of the weight-gradient GEMMs that split their K (token) range
   const int64_t tk = (int64_t)tok;
   const uint64_t dwp = std::max({split_ws_bytes(x.h, x.f_t, tk), split_ws_bytes(2 * x.f_t, x.h, tk),
-                                 split_ws_bytes(x.h, x.a_t * x.d, tk), split_ws_bytes(qkv_cols(x), x.h, tk)});
+                                 split_ws_bytes(x.h, x.a_t * x.d, tk), split_ws_bytes(qkv_cols(x), x.h, tk),
+                                 split_ws_bytes(tk, x.a_t * x.d, x.h, false)});   // and the O dX GEMM
   w.dwpart = dwp ? cv.take(dwp) : 0;
   w.total = cv.used;
   return w;
@@ -614,14 +616,16 @@ int run_gemm(const char* name, hipStream_t s, int64_t M, int64_t N, int64_t K, O
   p.A = A;
   p.B = B;
   p.epi = e;
-  if (e.kind == EpiKind::AccF32 && split_ws) {
-    p.k_splits = gemm_ksplits(M, N, K);
+  const bool acc = e.kind == EpiKind::AccF32;
+  if ((acc || e.kind == EpiKind::StoreBF16) && split_ws) {
+    p.k_splits = gemm_ksplits(M, N, K, acc);
     p.partial = split_ws;
   }
   int rc = launch(name, s, [&] { return gemm(p, la, lb, s); });
   if (rc || p.k_splits <= 1) return rc;
   return launch("gemm_splitk_reduce", s, [&] {
-    return gemm_split_reduce(static_cast<float*>(e.c), e.ldc, split_ws, M, N, p.k_splits, s);
+    return acc ? gemm_split_reduce(static_cast<float*>(e.c), e.ldc, split_ws, M, N, p.k_splits, s)
+               : gemm_split_store(static_cast<uint16_t*>(e.c), e.ldc, split_ws, M, N, p.k_splits, s);
   });
 }
 
@@ -892,7 +896,7 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
     // attention output projection
     const RowSrc dh1_full = gathered(dh1, pi.sp_peer_dh1, x);
     if ((r = run_gemm("gemm_o_dx", s, tok, nq, x.h, op(dh1_full, tok), Layout::KC, op(RowSrc::plain(w->o, nq), nq),
-                      Layout::MN, epi_store(dctx, nq))))
+                      Layout::MN, epi_store(dctx, nq), dwpart)))
       return r;
     if ((r = run_gemm("gemm_o_dw", s, x.h, nq, tok, op(dh1_full, x.h), Layout::MN,
                       op(RowSrc::plain(sptr(st, L4D_STASH_CTX), nq), nq), Layout::MN, epi_acc(dw->o, nq), dwpart)))

@@ -913,7 +913,8 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave: scalar code for wave-level decisions
   // AccF32 with a split K range: the grid is k_splits copies of the tile grid,
   // part-major after the XCD remap, so an XCD's neighbouring tiles share a part.
-  const int parts = KIND == EpiKind::AccF32 && p.k_splits > 1 ? p.k_splits : 1;
+  constexpr bool kSplittable = KIND == EpiKind::AccF32 || KIND == EpiKind::StoreBF16;
+  const int parts = kSplittable && p.k_splits > 1 ? p.k_splits : 1;
   const int pid_all = xcd_remap(blockIdx.x, gridDim.x);
   const int tiles = static_cast<int>(gridDim.x) / parts;
   const int part = pid_all / tiles;
@@ -933,6 +934,10 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   if constexpr (KIND == EpiKind::AccF32) {
     cbase = part == 0 ? static_cast<float*>(p.epi.c) : p.partial + static_cast<int64_t>(part - 1) * p.M * p.N;
     ldc = part == 0 ? p.epi.ldc : p.N;
+  } else if constexpr (KIND == EpiKind::StoreBF16) {
+    // split: every part stores its fp32 sum; the reduce pass adds them and rounds to bf16
+    cbase = p.partial + static_cast<int64_t>(part) * p.M * p.N;
+    ldc = p.N;
   }
 
   f32x16 acc[4][NS];
@@ -947,7 +952,7 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   // K is a multiple of 2 * BK2 * parts (the host picks this kernel only then).
   mainloop64<LA, LB, WAVES, KIND == EpiKind::AccF32>(p, acc, tm, tn, part * n_st, n_st, a0, b0, a1, b1, wave,
                                                              lane, wm, ncol);
-  if constexpr (KIND == EpiKind::AccF32) {
+  if (KIND == EpiKind::AccF32 || (KIND == EpiKind::StoreBF16 && parts > 1)) {
     acc_store_f32<NS>(acc, p, cbase, ldc, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
   } else {
     __syncthreads();   // every wave is done reading the stages
@@ -972,7 +977,8 @@ hipError_t launch(const GemmParams& p, hipStream_t stream, int variant) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = p.B.split_rows ? (p.B.split_rows + 127) / 128 : (p.N + BN - 1) / BN;
   const int parts = p.k_splits > 1 ? p.k_splits : 1;
-  if (parts > 1 && (KIND != EpiKind::AccF32 || p.K % (2 * BK2 * parts) != 0 || !p.partial))
+  if (parts > 1 && ((KIND != EpiKind::AccF32 && KIND != EpiKind::StoreBF16) || p.K % (2 * BK2 * parts) != 0 ||
+                    !p.partial))
     return hipErrorInvalidValue;
   const dim3 grid(tiles_m * tiles_n * parts);
   if (variant == 0) variant = gemm_variant_env();
@@ -1043,12 +1049,44 @@ __global__ void __launch_bounds__(256) split_reduce_kernel(float* __restrict__ c
   }
   *cp = v;
 }
+// C (bf16) = partial[0] + partial[1] + ..., four columns per thread.
+__global__ void __launch_bounds__(256) split_store_kernel(uint16_t* __restrict__ c, int64_t ldc,
+                                                         const float* __restrict__ part, int64_t M, int64_t N,
+                                                         int32_t n_part) {
+  const int64_t n4 = N / 4;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= M * n4) return;
+  const int64_t m = i / n4, j = (i - m * n4) * 4;
+  float4 v = *reinterpret_cast<const float4*>(part + m * N + j);
+  for (int s = 1; s < n_part; ++s) {
+    const float4 q = *reinterpret_cast<const float4*>(part + static_cast<int64_t>(s) * M * N + m * N + j);
+    v.x += q.x;
+    v.y += q.y;
+    v.z += q.z;
+    v.w += q.w;
+  }
+  uint16_t* o = c + m * ldc + j;
+  o[0] = f2bf(v.x);
+  o[1] = f2bf(v.y);
+  o[2] = f2bf(v.z);
+  o[3] = f2bf(v.w);
+}
 }  // namespace
 
-int gemm_ksplits(int64_t M, int64_t N, int64_t K) {
+hipError_t gemm_split_store(uint16_t* c, int64_t ldc, const float* partial, int64_t M, int64_t N, int32_t splits,
+                            hipStream_t stream) {
+  if (splits <= 1 || M <= 0 || N <= 0) return hipSuccess;
+  const int64_t n = M * (N / 4);
+  hipLaunchKernelGGL(split_store_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, c, ldc,
+                     partial, M, N, splits);
+  return hipGetLastError();
+}
+
+int gemm_ksplits(int64_t M, int64_t N, int64_t K, bool acc_f32) {
   // Model: a wave of 256 tiles of full K takes T = 2*256*256*K / (1 PFLOP/s / 256 CUs);
   // s parts take ceil(tiles*s / 256) waves of T/s, plus writing and reading the
-  // s - 1 fp32 partials at about 4 TB/s.  Pick the cheapest s of 1..4.
+  // fp32 partials at about 4 TB/s (s - 1 of them when part 0 accumulates into an
+  // fp32 C, all s when the result is stored as bf16).  Pick the cheapest s of 1..4.
   const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   const double t_wave = 2.0 * BM * BN * static_cast<double>(K) / (1e15 / 256.0);
   int best = 1;
@@ -1056,7 +1094,8 @@ int gemm_ksplits(int64_t M, int64_t N, int64_t K) {
   for (int s = 1; s <= 4; ++s) {
     if (K % (2 * BK2 * s) != 0 || N % 4 != 0) continue;
     const double waves = static_cast<double>((tiles * s + 255) / 256);
-    const double t = waves * t_wave / s + (s - 1) * 2.0 * 4.0 * static_cast<double>(M) * N / 4e12;
+    const int n_part = s == 1 ? 0 : (acc_f32 ? s - 1 : s);
+    const double t = waves * t_wave / s + n_part * 2.0 * 4.0 * static_cast<double>(M) * N / 4e12;
     if (t < best_t * 0.97) {       // a split has to win by a margin
       best_t = t;
       best = s;

@@ -95,10 +95,11 @@ struct GemmParams {
   int32_t M, N, K;
   Operand A, B;
   EpiParams epi;
-  // AccF32 only: the K range is cut into k_splits equal parts (0 or 1 = none).
-  // Part 0 accumulates into C; part s > 0 stores its fp32 sum to
-  // partial + (s - 1) M N (row-major, ld N), which gemm_split_reduce then adds
-  // to C in order s = 1, 2, ...
+  // AccF32 and StoreBF16 only: the K range is cut into k_splits equal parts
+  // (0 or 1 = none).  AccF32: part 0 accumulates into C; part s > 0 stores its
+  // fp32 sum to partial + (s - 1) M N (row-major, ld N), which
+  // gemm_split_reduce then adds to C in order s = 1, 2, ...  StoreBF16: part s
+  // stores to partial + s M N and gemm_split_store writes bf16(sum) to C.
   int32_t k_splits;
   float* partial;
 };
@@ -106,10 +107,13 @@ struct GemmParams {
 hipError_t gemm(const GemmParams& p, Layout la, Layout lb, hipStream_t stream);
 // Parts the K range of an fp32-accumulate GEMM is cut into when one tile per
 // workgroup would leave much of the chip idle (1 = no split).
-int gemm_ksplits(int64_t M, int64_t N, int64_t K);
+int gemm_ksplits(int64_t M, int64_t N, int64_t K, bool acc_f32);
 // C[m][n] += sum over s of partial[s][m][n], s = 0 .. splits - 2, in that order.
 hipError_t gemm_split_reduce(float* c, int64_t ldc, const float* partial, int64_t M, int64_t N, int32_t splits,
                              hipStream_t stream);
+// C (bf16) = sum over s of partial[s], s = 0 .. splits - 1, in that order.
+hipError_t gemm_split_store(uint16_t* c, int64_t ldc, const float* partial, int64_t M, int64_t N, int32_t splits,
+                            hipStream_t stream);
 
 // ---------------------------------------------------------------- row-wise kernels
 
