@@ -1087,6 +1087,10 @@ int gemm_ksplits(int64_t M, int64_t N, int64_t K, bool acc_f32) {
   // s parts take ceil(tiles*s / 256) waves of T/s, plus writing and reading the
   // fp32 partials at about 4 TB/s (s - 1 of them when part 0 accumulates into an
   // fp32 C, all s when the result is stored as bf16).  Pick the cheapest s of 1..4.
+  // The rate is deliberately low: the chip is power-limited, so a wave that
+  // leaves CUs idle runs at a higher clock than tile counting suggests (the
+  // 160-tile qkv weight gradient of the 70B shard was no faster in 4 parts),
+  // and only clearly under-filled grids (128 tiles) split.
   const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   const double t_wave = 2.0 * BM * BN * static_cast<double>(K) / (1e15 / 256.0);
   int best = 1;
