@@ -747,11 +747,10 @@ extern "C" int llama_layer_fwd(const l4d_model* m, const l4d_parallel* p, const 
     int r;
     if ((r = launch("rope_table", s, [&] { return rope_table(rope, x.qmap, (int32_t)x.s_c, (int32_t)x.d, x.base, s); })))
       return r;
-    // stash x (norm-1 input) and norm-1
-    HIP_TRY(hipMemcpyAsync(sptr(st, L4D_STASH_X), x_in, st->bytes[L4D_STASH_X], hipMemcpyDeviceToDevice, s));
+    // norm-1, stashing its input x as it goes
     if ((r = launch("rmsnorm_fwd", s, [&] {
            return rmsnorm_fwd(static_cast<const uint16_t*>(x_in), static_cast<const uint16_t*>(w->norm1),
-                              sptr(st, L4D_STASH_XN1), x.b * x.s_sp, (int32_t)x.h, x.eps, s);
+                              sptr(st, L4D_STASH_XN1), x.b * x.s_sp, (int32_t)x.h, x.eps, s, sptr(st, L4D_STASH_X));
          })))
       return r;
     // [Q|K|V] = xn1_full W_qkv^T, RoPE on Q, K
@@ -1081,10 +1080,9 @@ extern "C" int lm_head_fwd(const l4d_model* m, const l4d_parallel* p, const void
   if ((rc = stash_reserve_sized(A, x, kHeadStash, L4D_HEAD_COUNT, bytes, -1, &st))) return rc;
   auto body = [&]() -> int {
     int r;
-    HIP_TRY(hipMemcpyAsync(sptr<void>(st, L4D_HEAD_X), x_in, sp, hipMemcpyDeviceToDevice, s));
     if ((r = launch("rmsnorm_fwd", s, [&] {
            return rmsnorm_fwd(static_cast<const uint16_t*>(x_in), static_cast<const uint16_t*>(w_norm),
-                              sptr(st, L4D_HEAD_XN), x.b * x.s_sp, (int32_t)x.h, x.eps, s);
+                              sptr(st, L4D_HEAD_XN), x.b * x.s_sp, (int32_t)x.h, x.eps, s, sptr(st, L4D_HEAD_X));
          })))
       return r;
     EpiParams e{};

@@ -117,9 +117,10 @@ hipError_t gemm_split_store(uint16_t* c, int64_t ldc, const float* partial, int6
 
 // ---------------------------------------------------------------- row-wise kernels
 
-// y = bf16(gain * x * rsqrt(mean(x^2) + eps)), one row of h per wave.
+// y = bf16(gain * x * rsqrt(mean(x^2) + eps)), one row of h per wave; x is
+// also copied to x_copy when that is not null.
 hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* gain, uint16_t* y, int64_t rows,
-                       int32_t h, float eps, hipStream_t stream);
+                       int32_t h, float eps, hipStream_t stream, uint16_t* x_copy = nullptr);
 // dx = bf16(dres + d rmsnorm/dx . dy);  partial[blk][h] = sum over the block's rows of dy*xhat.
 hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const uint16_t* dy,
                        const uint16_t* dres, uint16_t* dx, float* partial, int32_t n_partial,

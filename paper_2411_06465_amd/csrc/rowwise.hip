@@ -47,8 +47,8 @@ constexpr int kMaxChunks = 16;   // h <= 64 lanes * 16 chunks * 8 = 8192
 
 __global__ void __launch_bounds__(256) rmsnorm_fwd_kernel(const uint16_t* __restrict__ x,
                                                           const uint16_t* __restrict__ gain,
-                                                          uint16_t* __restrict__ y, int64_t rows,
-                                                          int32_t h, float eps) {
+                                                          uint16_t* __restrict__ y, uint16_t* __restrict__ x_copy,
+                                                          int64_t rows, int32_t h, float eps) {
   const int lane = threadIdx.x & 63;
   const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
@@ -65,6 +65,14 @@ __global__ void __launch_bounds__(256) rmsnorm_fwd_kernel(const uint16_t* __rest
       unpack8(v[it], f);
 #pragma unroll
       for (int j = 0; j < 8; ++j) ss += f[j] * f[j];
+    }
+  }
+  if (x_copy) {     // the input, kept for the backward
+    u32x4* cr = reinterpret_cast<u32x4*>(x_copy + row * h);
+#pragma unroll
+    for (int it = 0; it < kMaxChunks; ++it) {
+      const int c = lane + 64 * it;
+      if (c < nch) cr[c] = v[it];
     }
   }
   const float rstd = rsqrtf(wave_sum(ss) / h + eps);
@@ -103,20 +111,39 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[it][j] = 0.f;
   const u32x4* gr = reinterpret_cast<const u32x4*>(gain);
-  int parity = 0;
-  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x, parity ^= 1) {
+  u32x4 gv[CPT], xv[CPT], dv[CPT], rv[CPT], xn[CPT], dn[CPT], rn[CPT];
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  // row `row`'s x, dy and residual gradient into (a, b, r)
+  auto load_row = [&](int64_t row, u32x4 (&a)[CPT], u32x4 (&b)[CPT], u32x4 (&r)[CPT]) __attribute__((always_inline)) {
     const u32x4* xr = reinterpret_cast<const u32x4*>(x + row * h);
     const u32x4* dr = reinterpret_cast<const u32x4*>(dy + row * h);
-    u32x4 xv[CPT], dv[CPT], gv[CPT];
+    const u32x4* rr = dres ? reinterpret_cast<const u32x4*>(dres + row * h) : nullptr;
 #pragma unroll
     for (int it = 0; it < CPT; ++it) {
       const int c = tid + 256 * it;
       if (c < nch) {
-        xv[it] = xr[c];
-        dv[it] = dr[c];
-        gv[it] = gr[c];
+        a[it] = xr[c];
+        b[it] = dr[c];
+        r[it] = rr ? rr[c] : zero;
       }
     }
+  };
+#pragma unroll
+  for (int it = 0; it < CPT; ++it) {
+    const int c = tid + 256 * it;
+    if (c < nch) gv[it] = gr[c];
+  }
+  int parity = 0;
+  if (static_cast<int64_t>(blockIdx.x) < rows) load_row(blockIdx.x, xn, dn, rn);
+  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x, parity ^= 1) {
+#pragma unroll
+    for (int it = 0; it < CPT; ++it) {
+      xv[it] = xn[it];
+      dv[it] = dn[it];
+      rv[it] = rn[it];
+    }
+    // the next row's loads fly under this row's reductions and stores
+    if (row + gridDim.x < rows) load_row(row + gridDim.x, xn, dn, rn);
     float ss = 0.f, dot = 0.f;
 #pragma unroll
     for (int it = 0; it < CPT; ++it) {
@@ -144,7 +171,6 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
     dot = (sums[parity][0][1] + sums[parity][1][1]) + (sums[parity][2][1] + sums[parity][3][1]);
     const float rstd = rsqrtf(ss / h + eps);
     const float c_mean = dot * rstd / h;        // mean over the row of (gain*dy) * xhat
-    const u32x4* rr = dres ? reinterpret_cast<const u32x4*>(dres + row * h) : nullptr;
     u32x4* out = reinterpret_cast<u32x4*>(dx + row * h);
 #pragma unroll
     for (int it = 0; it < CPT; ++it) {
@@ -154,13 +180,12 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
         unpack8(xv[it], f);
         unpack8(dv[it], d);
         unpack8(gv[it], g);
-        if (rr) unpack8(rr[c], r);
+        unpack8(rv[it], r);      // zeros without a residual gradient
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const float xh = f[j] * rstd;
           acc[it][j] += d[j] * xh;
-          const float v = rstd * (g[j] * d[j] - xh * c_mean);
-          r[j] = rr ? r[j] + v : v;
+          r[j] += rstd * (g[j] * d[j] - xh * c_mean);
         }
         out[c] = pack8(r);
       }
@@ -437,10 +462,10 @@ __global__ void __launch_bounds__(256) embed_bwd_kernel(const int64_t* __restric
 }  // namespace
 
 hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* gain, uint16_t* y, int64_t rows, int32_t h,
-                       float eps, hipStream_t stream) {
+                       float eps, hipStream_t stream, uint16_t* x_copy) {
   if (rows <= 0) return hipSuccess;
   hipLaunchKernelGGL(rmsnorm_fwd_kernel, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream,
-                     x, gain, y, rows, h, eps);
+                     x, gain, y, x_copy, rows, h, eps);
   return hipGetLastError();
 }
 
