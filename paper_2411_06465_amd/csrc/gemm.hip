@@ -55,7 +55,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int BM = 256, BN = 256, BK = 32;
 constexpr int TILE_BYTES = 256 * BK * 2;     // 16 KB per operand per stage
-constexpr int GROUP_M = 8;
+constexpr int GROUP_M = 4;
 
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
