@@ -470,7 +470,7 @@ hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* gain, uint16_t* y, int
 }
 
 int32_t rmsnorm_bwd_partials(int64_t rows) {
-  return static_cast<int32_t>(rows < 1024 ? rows : 1024);     // one block per row, up to four per CU
+  return static_cast<int32_t>(rows < 256 ? rows : 256);     // one block per row, one per CU
 }
 
 hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const uint16_t* dy, const uint16_t* dres,
