@@ -125,7 +125,8 @@ hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* gain, uint16_t* y, int
 hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const uint16_t* dy,
                        const uint16_t* dres, uint16_t* dx, float* partial, int32_t n_partial,
                        int64_t rows, int32_t h, float eps, hipStream_t stream);
-// out[j] += sum_i partial[i][j]; partial is overwritten (used as scratch).
+// out[j] += sum_i partial[i][j] in a fixed order; with more than 256 rows partial
+// is overwritten (used as scratch).
 hipError_t reduce_rows_add(float* partial, int32_t n_partial, int32_t h, float* out, hipStream_t stream);
 int32_t rmsnorm_bwd_partials(int64_t rows);
 

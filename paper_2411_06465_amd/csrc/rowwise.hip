@@ -229,6 +229,30 @@ __global__ void __launch_bounds__(256) reduce_slices_kernel(float* __restrict__ 
     partial[static_cast<int64_t>(r0) * h + col] = (s4[0][lane] + s4[1][lane]) + (s4[2][lane] + s4[3][lane]);
 }
 
+// One level for at most 256 partial rows: a block per 64 columns, its 4 waves
+// taking every 4th row (four loads in flight each), then out += the column sums.
+__global__ void __launch_bounds__(256) reduce_all_kernel(const float* __restrict__ partial, int32_t n, int32_t h,
+                                                        float* __restrict__ out) {
+  __shared__ float s4[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = blockIdx.x * 64 + lane;
+  float s = 0.f;
+  if (col < h) {
+    int i = wave;
+    for (; i + 12 < n; i += 16) {
+      const float a = partial[static_cast<int64_t>(i) * h + col];
+      const float b = partial[static_cast<int64_t>(i + 4) * h + col];
+      const float c = partial[static_cast<int64_t>(i + 8) * h + col];
+      const float d = partial[static_cast<int64_t>(i + 12) * h + col];
+      s += (a + b) + (c + d);
+    }
+    for (; i < n; i += 4) s += partial[static_cast<int64_t>(i) * h + col];
+  }
+  s4[wave][lane] = s;
+  __syncthreads();
+  if (wave == 0 && col < h) out[col] += (s4[0][lane] + s4[1][lane]) + (s4[2][lane] + s4[3][lane]);
+}
+
 __global__ void __launch_bounds__(256) add_slices_kernel(const float* __restrict__ partial, int32_t n_slices,
                                                          int32_t h, float* __restrict__ out) {
   const int col = blockIdx.x * 256 + threadIdx.x;
@@ -490,6 +514,10 @@ hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const uint16_t* 
 
 hipError_t reduce_rows_add(float* partial, int32_t n_partial, int32_t h, float* out, hipStream_t stream) {
   if (n_partial <= 0) return hipSuccess;
+  if (n_partial <= 256) {
+    hipLaunchKernelGGL(reduce_all_kernel, dim3((h + 63) / 64), dim3(256), 0, stream, partial, n_partial, h, out);
+    return hipGetLastError();
+  }
   const int slices = (n_partial + 63) / 64;
   hipLaunchKernelGGL(reduce_slices_kernel, dim3((h + 63) / 64, slices), dim3(256), 0, stream, partial, n_partial, h);
   hipLaunchKernelGGL(add_slices_kernel, dim3((h + 255) / 256), dim3(256), 0, stream, partial, slices, h, out);
