@@ -92,16 +92,16 @@ typedef struct {
  * tp*cp*pp*dp is the GPU count implied by dp >= 1.  Exact integer arithmetic. */
 int mem_estimate(const l4d_model* model, const l4d_parallel* par, l4d_mem* out);
 
-/* Verdict of an estimate against the device memory (Sec. 4.1): the paper
+/* Fit of an estimate in the device memory (Sec. 4.1): the paper
  * finds that a configuration whose estimated total is at most 80% of the GPU
  * memory trains (temporary buffers and fragmentation fit in the rest), one
  * above 100% runs out of memory, and one in between may go either way.
  *   est: a filled l4d_mem (its total_bytes is used);
  *   device_bytes: the GPU memory in bytes (the paper's 40 GB and 94 GB read as
- *   40 and 94 GiB);  *verdict: one of the values below.
+ *   40 and 94 GiB);  *fit: one of the values below.
  * L4D_EINVAL for NULL pointers or device_bytes == 0.  Host only. */
 enum { L4D_FITS = 0, L4D_NEAR_LIMIT = 1, L4D_OOM = 2 };
-int mem_verdict(const l4d_mem* est, uint64_t device_bytes, int* verdict);
+int mem_fit(const l4d_mem* est, uint64_t device_bytes, int* fit);
 
 /* ------------------------------------------------------------------------
  * Arena and activation stash (Sec. 3.2)

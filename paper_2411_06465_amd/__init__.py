@@ -80,7 +80,7 @@ def lib():
         sig = {
             "l4d_last_error": ([], C.c_char_p),
             "mem_estimate": ([C.POINTER(Model), C.POINTER(Parallel), C.POINTER(Mem)], C.c_int),
-            "mem_verdict": ([C.POINTER(Mem), u64, C.POINTER(C.c_int)], C.c_int),
+            "mem_fit": ([C.POINTER(Mem), u64, C.POINTER(C.c_int)], C.c_int),
             "l4d_arena_create": ([P, u64, C.POINTER(P)], C.c_int),
             "l4d_arena_destroy": ([P], C.c_int),
             "l4d_arena_stats": ([P, C.POINTER(u64), C.POINTER(u64), C.POINTER(u64)], C.c_int),
@@ -148,16 +148,16 @@ def mem_estimate(model, par):
     return {n: getattr(out, n) for n, _ in Mem._fields_}
 
 
-VERDICTS = {0: "fits", 1: "near_limit", 2: "oom"}
+FIT_CLASSES = {0: "fits", 1: "near_limit", 2: "oom"}
 
 
-def mem_verdict(est, device_bytes):
+def mem_fit(est, device_bytes):
     """'fits' (estimate <= 80% of device_bytes), 'near_limit' (<= 100%) or 'oom';
     `est` is a dict from mem_estimate."""
     m = Mem(*[est[n] for n, _ in Mem._fields_])
     out = C.c_int()
-    _check(lib().mem_verdict(C.byref(m), device_bytes, C.byref(out)))
-    return VERDICTS[out.value]
+    _check(lib().mem_fit(C.byref(m), device_bytes, C.byref(out)))
+    return FIT_CLASSES[out.value]
 
 
 # ------------------------------------------------------------------ arena / stash

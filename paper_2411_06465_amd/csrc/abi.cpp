@@ -223,11 +223,11 @@ extern "C" int mem_estimate(const l4d_model* m, const l4d_parallel* p, l4d_mem* 
   return L4D_OK;
 }
 
-extern "C" int mem_verdict(const l4d_mem* est, uint64_t device_bytes, int* verdict) {
-  if (!est || !verdict || device_bytes == 0) return fail(L4D_EINVAL, "est, verdict and device_bytes are required");
+extern "C" int mem_fit(const l4d_mem* est, uint64_t device_bytes, int* fit) {
+  if (!est || !fit || device_bytes == 0) return fail(L4D_EINVAL, "est, fit and device_bytes are required");
   // total <= 0.8 M  <=>  5 total <= 4 M, in 128-bit integers
   const unsigned __int128 t5 = (unsigned __int128)est->total_bytes * 5, m4 = (unsigned __int128)device_bytes * 4;
-  *verdict = t5 <= m4 ? L4D_FITS : (est->total_bytes <= device_bytes ? L4D_NEAR_LIMIT : L4D_OOM);
+  *fit = t5 <= m4 ? L4D_FITS : (est->total_bytes <= device_bytes ? L4D_NEAR_LIMIT : L4D_OOM);
   return L4D_OK;
 }
 

@@ -235,7 +235,7 @@ def test_adam_step_rejects_oversized_shard():
     assert "too large" in L.lib().l4d_last_error().decode()
 
 
-def test_mem_verdict_equals_the_oracle_on_every_printed_run():
+def test_mem_fit_equals_the_oracle_on_every_printed_run():
     gold = os.path.join(os.path.dirname(__file__), "golden")
     names = {"fits": "green", "near_limit": "yellow", "oom": "red"}
     arch = {"llama-3.1-8b": (4096, 32, 8, 14336, 32, 128256), "llama-3.1-70b": (8192, 64, 8, 28672, 80, 128256)}
@@ -248,7 +248,7 @@ def test_mem_verdict_equals_the_oracle_on_every_printed_run():
                 m = L.make_model(hidden=h, n_heads=a, n_kv_heads=k, ffn=ffn, n_layers=layers, vocab=v)
                 p = L.make_parallel(seq=c["seq"], micro_batch=c["mbs"], tp=c["tp"], cp=c["cp"], pp=c["pp"], dp=d)
                 est = L.mem_estimate(m, p)
-                got = L.mem_verdict(est, c["gpu_mem_gb"] << 30)
+                got = L.mem_fit(est, c["gpu_mem_gb"] << 30)
                 want = M.oom_class(M.estimate(h, a, k, ffn, layers, v, s=c["seq"], b=c["mbs"], t=c["tp"],
                                               c=c["cp"], p=c["pp"], d=d)["total"], c["gpu_mem_gb"] << 30)
                 assert names[got] == want == c["colour"], c
@@ -256,8 +256,8 @@ def test_mem_verdict_equals_the_oracle_on_every_printed_run():
     assert n == 908
     gib = 1 << 30
     base = L.mem_estimate(*model_par(TINY))
-    for total, verdict in ((32 * gib, "fits"), (32 * gib + 1, "near_limit"), (40 * gib, "near_limit"),
-                           (40 * gib + 1, "oom"), ((1 << 64) - 1, "oom")):
-        assert L.mem_verdict(dict(base, total_bytes=total), 40 * gib) == verdict
+    for total, fit in ((32 * gib, "fits"), (32 * gib + 1, "near_limit"), (40 * gib, "near_limit"),
+                       (40 * gib + 1, "oom"), ((1 << 64) - 1, "oom")):
+        assert L.mem_fit(dict(base, total_bytes=total), 40 * gib) == fit
     with pytest.raises(L.L4DError):
-        L.mem_verdict(base, 0)
+        L.mem_fit(base, 0)
