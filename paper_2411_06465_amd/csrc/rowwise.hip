@@ -284,36 +284,46 @@ __global__ void __launch_bounds__(256) xent_rows_kernel(
     const uint16_t* __restrict__ logits, int32_t v_t, int64_t v0, const int64_t* __restrict__ targets,
     const float* __restrict__ peer_lse, const float* __restrict__ peer_z, float grad_scale,
     float* __restrict__ loss, uint16_t* __restrict__ dlogits) {
-  __shared__ float red[4];
+  __shared__ float red_m[4], red_s[4];
   __shared__ float bcast;
   const int64_t row = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const u32x4* lr = reinterpret_cast<const u32x4*>(logits + row * v_t);
   const int nch = v_t / 8;
-  float mx = -INFINITY;
+  // one read of the row: running maximum and the sum of exponentials relative to it
+  float mx = -INFINITY, se = 0.f;
   for (int c = threadIdx.x; c < nch; c += 256) {
     float f[8];
     unpack8(lr[c], f);
+    float m8 = f[0];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) mx = fmaxf(mx, f[j]);
-  }
-  mx = wave_max(mx);
-  if (lane == 0) red[wave] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  __syncthreads();
-  float se = 0.f;
-  for (int c = threadIdx.x; c < nch; c += 256) {
-    float f[8];
-    unpack8(lr[c], f);
+    for (int j = 1; j < 8; ++j) m8 = fmaxf(m8, f[j]);
+    if (m8 > mx) {
+      se *= __expf(mx - m8);       // 0 while mx is -inf
+      mx = m8;
+    }
 #pragma unroll
     for (int j = 0; j < 8; ++j) se += __expf(f[j] - mx);
   }
-  se = wave_sum(se);
-  if (lane == 0) red[wave] = se;
+  // combine (max, sum) pairs across the wave, then the four waves
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(mx, o, 64), s2 = __shfl_xor(se, o, 64);
+    const float m = fmaxf(mx, m2);
+    se = (mx == -INFINITY ? 0.f : se * __expf(mx - m)) + (m2 == -INFINITY ? 0.f : s2 * __expf(m2 - m));
+    mx = m;
+  }
+  if (lane == 0) {
+    red_m[wave] = mx;
+    red_s[wave] = se;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
-    float lse = mx + logf(red[0] + red[1] + red[2] + red[3]);
+    float m = fmaxf(fmaxf(red_m[0], red_m[1]), fmaxf(red_m[2], red_m[3]));
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) sum += red_m[w] == -INFINITY ? 0.f : red_s[w] * __expf(red_m[w] - m);
+    float lse = m + logf(sum);
     if (peer_lse) {
       const float p = peer_lse[row];
       const float hi = fmaxf(lse, p), lo = fminf(lse, p);
