@@ -412,8 +412,9 @@ def run_lm(w, steps, warmup):
 
 
 def cpu_baseline(w, seq):
-    """The oracle (float64 numpy, as written) on a bounded sample of the same
-    layer: same hidden/heads/FFN, sequence cut to `seq`."""
+    """The oracle (float64 numpy, as written) on the same layer: same
+    hidden/heads/FFN, sequence `seq` (the default 4096 is the whole workload,
+    about 10-20 s on a 16-thread host)."""
     from threadpoolctl import threadpool_info
     import workloads as W
     from oracle import layer as OL
@@ -432,8 +433,8 @@ def cpu_baseline(w, seq):
     flops, _, _ = layer_flops(ws)
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"{ws.name}: full layer fwd+bwd at seq {seq} (h {w.hidden}, {w.n_heads}/{w.n_kv_heads} heads, "
-                      f"FFN {w.ffn}), float64 numpy, {dt:.1f} s wall"}
+            "sample": f"{ws.name}: one layer fwd+bwd at seq {seq}{' (the whole workload)' if seq == w.seq else ''} "
+                      f"(h {w.hidden}, {w.n_heads}/{w.n_kv_heads} heads, FFN {w.ffn}), float64 numpy, {dt:.1f} s wall"}
 
 
 def main():
@@ -443,7 +444,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-others", action="store_true")
-    ap.add_argument("--cpu-seq", type=int, default=2048)
+    ap.add_argument("--cpu-seq", type=int, default=4096, help="sequence of the oracle's CPU run (4096: the whole layer)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
     ap.add_argument("--optimizer-only", action="store_true",
                     help="time only the Adam step over the 70B optimizer shard and print its object")
