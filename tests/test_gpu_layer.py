@@ -30,6 +30,11 @@ CASES = {
     # 1024 tokens over few weight-gradient tiles: those GEMMs cut their token range in 4 parts
     # (d128-s384: in 3), each part summed in fp32 and added to the accumulator in order
     "d128-s1024-splitk": W.LayerWorkload("d128-s1024", 512, 4, 2, 1376, 1024, rope_base=5e5),
+    # GQA group 4 per rank at TP2 (dK/dV split over query heads) with split weight gradients
+    "gqa4-tp2-s768": W.LayerWorkload("gqa4-tp2", 1024, 8, 2, 2816, 768, tp=2, tp_rank=0, n_gpus=2, rope_base=5e5),
+    # CP2 with two sequences per micro-batch: remote key segments in the heaviest-first dK/dV order
+    "cp2-b2-s1024": W.LayerWorkload("cp2-b2", 512, 4, 4, 1376, 1024, micro_batch=2, cp=2, cp_rank=1, n_gpus=2,
+                                    rope_base=1e4),
 }
 
 
