@@ -154,6 +154,9 @@ int l4d_stash_release(l4d_arena* arena, l4d_stash* stash);
  * on top of the stash (so that callers can size an arena). */
 int l4d_layer_workspace_bytes(const l4d_model* model, const l4d_parallel* par,
                               uint64_t* fwd_bytes, uint64_t* bwd_bytes);
+/* Workspace lm_head_xent takes from the arena: the bf16 logits, plus an fp32
+ * n_tokens x hidden buffer when vocab_shard is at least 1024 and not a multiple
+ * of 128 (d_hidden is then summed in fp32 over two kernels). */
 int l4d_lm_head_workspace_bytes(int64_t n_tokens, int64_t hidden, int64_t vocab_shard,
                                 uint64_t* bytes);
 

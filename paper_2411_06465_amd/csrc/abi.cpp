@@ -556,9 +556,16 @@ extern "C" int l4d_layer_workspace_bytes(const l4d_model* m, const l4d_parallel*
   return L4D_OK;
 }
 
+namespace {
+// A K-contiguous x N-contiguous GEMM whose K is long but not a multiple of 128
+// (the LM head's d_hidden over a vocabulary shard) runs its first K - K % 128 on
+// the BK = 64 kernel and the rest on the ragged-K kernel, summing in fp32.
+bool ragged_k_split(int64_t K) { return K % 128 != 0 && K >= 1024; }
+}  // namespace
+
 extern "C" int l4d_lm_head_workspace_bytes(int64_t n, int64_t h, int64_t v_t, uint64_t* bytes) {
   if (n < 0 || h <= 0 || v_t <= 0) return fail(L4D_EINVAL, "bad LM-head sizes");
-  if (bytes) *bytes = align_up((uint64_t)n * v_t * 2);
+  if (bytes) *bytes = align_up((uint64_t)n * v_t * 2) + (ragged_k_split(v_t) ? align_up((uint64_t)n * h * 4) : 0);
   return L4D_OK;
 }
 
@@ -966,9 +973,12 @@ extern "C" int lm_head_xent(int64_t n, int64_t h, int64_t v_t, int64_t v0, const
   if (n == 0) return L4D_OK;
   hipStream_t s = static_cast<hipStream_t>(stream_ptr);
   Workspace ws;
-  int rc = take_ws(A, (uint64_t)n * v_t * 2, ws);
+  const uint64_t logit_bytes = align_up((uint64_t)n * v_t * 2);
+  const bool split_k = ragged_k_split(v_t);
+  int rc = take_ws(A, logit_bytes + (split_k ? (uint64_t)n * h * 4 : 0), ws);
   if (rc) return rc;
   uint16_t* logits = reinterpret_cast<uint16_t*>(A->base + ws.off);
+  float* dh_f32 = split_k ? reinterpret_cast<float*>(A->base + ws.off + logit_bytes) : nullptr;
   if ((rc = run_gemm("gemm_lm_logits", s, n, v_t, h, op(RowSrc::plain(hidden, h), n), Layout::KC,
                      op(RowSrc::plain(w_lm, h), v_t), Layout::KC, epi_store(logits, v_t))))
     return rc;
@@ -976,9 +986,29 @@ extern "C" int lm_head_xent(int64_t n, int64_t h, int64_t v_t, int64_t v0, const
          return xent_rows(logits, n, (int32_t)v_t, v0, targets, peer_lse, peer_z, grad_scale, loss, logits, s);
        })))
     return rc;
-  if ((rc = run_gemm("gemm_lm_dx", s, n, h, v_t, op(RowSrc::plain(logits, v_t), n), Layout::KC,
-                     op(RowSrc::plain(w_lm, h), h), Layout::MN, epi_store(d_hidden, h))))
-    return rc;
+  if (!split_k) {
+    if ((rc = run_gemm("gemm_lm_dx", s, n, h, v_t, op(RowSrc::plain(logits, v_t), n), Layout::KC,
+                       op(RowSrc::plain(w_lm, h), h), Layout::MN, epi_store(d_hidden, h))))
+      return rc;
+  } else {
+    // d_hidden = dlogits[:, :K1] W_lm[:K1] + dlogits[:, K1:] W_lm[K1:] in fp32, then bf16
+    const int64_t k1 = v_t - v_t % 128, k2 = v_t - k1;
+    EpiParams ef{};
+    ef.kind = EpiKind::StoreF32;
+    ef.c = dh_f32;
+    ef.ldc = h;
+    if ((rc = run_gemm("gemm_lm_dx", s, n, h, k1, op(RowSrc::plain(logits, v_t), n), Layout::KC,
+                       op(RowSrc::plain(w_lm, h), h), Layout::MN, ef)))
+      return rc;
+    if ((rc = run_gemm("gemm_lm_dx_tail", s, n, h, k2, op(RowSrc::plain(logits + k1, v_t), n), Layout::KC,
+                       op(RowSrc::plain(static_cast<const uint16_t*>(w_lm) + k1 * h, h), h), Layout::MN,
+                       epi_acc(dh_f32, h))))
+      return rc;
+    if ((rc = launch("gemm_splitk_reduce", s, [&] {
+           return gemm_split_store(static_cast<uint16_t*>(d_hidden), h, dh_f32, n, h, 1, s);
+         })))
+      return rc;
+  }
   return run_gemm("gemm_lm_dw", s, v_t, h, n, op(RowSrc::plain(logits, v_t), v_t), Layout::MN,
                   op(RowSrc::plain(hidden, h), h), Layout::MN, epi_acc(d_w, h));
 }

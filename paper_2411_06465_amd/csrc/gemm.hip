@@ -1022,6 +1022,8 @@ hipError_t gemm_variant(const GemmParams& p, Layout la, Layout lb, hipStream_t s
     if (k == E::SwiGLUBwd) return launch<L::KC, L::MN, E::SwiGLUBwd, 128>(p, stream, variant);
     if (k == E::ResidualSP) return launch<L::KC, L::MN, E::ResidualSP, 128>(p, stream, variant);
     if (k == E::StoreBF16) return launch<L::KC, L::MN, E::StoreBF16, 128>(p, stream, variant);
+    if (k == E::StoreF32) return launch<L::KC, L::MN, E::StoreF32, 128>(p, stream, variant);
+    if (k == E::AccF32) return launch<L::KC, L::MN, E::AccF32, 128>(p, stream, variant);
   } else if (la == L::MN && lb == L::MN) {
     if (k == E::AccF32) return launch<L::MN, L::MN, E::AccF32, 128>(p, stream, variant);
   }
@@ -1075,7 +1077,7 @@ __global__ void __launch_bounds__(256) split_store_kernel(uint16_t* __restrict__
 
 hipError_t gemm_split_store(uint16_t* c, int64_t ldc, const float* partial, int64_t M, int64_t N, int32_t splits,
                             hipStream_t stream) {
-  if (splits <= 1 || M <= 0 || N <= 0) return hipSuccess;
+  if (splits < 1 || M <= 0 || N <= 0) return hipSuccess;
   const int64_t n = M * (N / 4);
   hipLaunchKernelGGL(split_store_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, c, ldc,
                      partial, M, N, splits);

@@ -111,7 +111,8 @@ int gemm_ksplits(int64_t M, int64_t N, int64_t K, bool acc_f32);
 // C[m][n] += sum over s of partial[s][m][n], s = 0 .. splits - 2, in that order.
 hipError_t gemm_split_reduce(float* c, int64_t ldc, const float* partial, int64_t M, int64_t N, int32_t splits,
                              hipStream_t stream);
-// C (bf16) = sum over s of partial[s], s = 0 .. splits - 1, in that order.
+// C (bf16) = sum over s of partial[s], s = 0 .. splits - 1, in that order
+// (splits = 1: the fp32 partial rounded to bf16).
 hipError_t gemm_split_store(uint16_t* c, int64_t ldc, const float* partial, int64_t M, int64_t N, int32_t splits,
                             hipStream_t stream);
 

@@ -175,7 +175,9 @@ def test_workspace_sizes_are_reported():
     for w in LAYER_WORKLOADS.values():
         f, b = L.l4d_layer_workspace_bytes(*model_par(w))
         assert f > 0 and b > 0
-    assert L.l4d_lm_head_workspace_bytes(8192, 4096, 32064) == 8192 * 32064 * 2
+    # bf16 logits, plus an fp32 d_hidden when the vocabulary shard is not a multiple of 128
+    assert L.l4d_lm_head_workspace_bytes(8192, 4096, 32064) == 8192 * 32064 * 2 + 8192 * 4096 * 4
+    assert L.l4d_lm_head_workspace_bytes(8192, 4096, 32000) == 8192 * 32000 * 2
 
 
 def test_layer_calls_validate_before_touching_the_device():

@@ -14,6 +14,8 @@ pytestmark = pytest.mark.gpu
 CASES = {
     "t1-small": W.LMHeadWorkload("lm-t1", 256, 256, 1000),
     "t4-ragged": W.LMHeadWorkload("lm-t4", 300, 512, 4000, tp=4, tp_rank=2),
+    # vocabulary shard 1288: d_hidden over the first 1280 on the BK = 64 kernel, the last 8 on the ragged one
+    "t2-split-k": W.LMHeadWorkload("lm-t2", 512, 512, 2576, tp=2, tp_rank=1),
 }
 
 
