@@ -1154,6 +1154,8 @@ extern "C" int lm_head_bwd(const l4d_model* m, const l4d_parallel* p, const void
   const uint64_t o_dl = cv.take((uint64_t)tok * v_t * 2), o_dxn = cv.take((uint64_t)rows_sp * x.h * 2);
   const uint64_t o_part = cv.take((uint64_t)npart * x.h * 4);
   const uint64_t o_send = (x.t > 1 && !dxn_send) ? cv.take((uint64_t)x.b * (x.t - 1) * x.s_sp * x.h * 2) : 0;
+  const bool split_k = ragged_k_split(v_t);
+  const uint64_t o_sum = split_k ? cv.take((uint64_t)tok * x.h * 4) : 0;
   Workspace ws;
   if ((rc = take_ws(A, cv.used, ws))) return rc;
   uint8_t* wsb = reinterpret_cast<uint8_t*>(A->base + ws.off);
@@ -1166,9 +1168,30 @@ extern "C" int lm_head_bwd(const l4d_model* m, const l4d_parallel* p, const void
        })))
     return rc;
   // d(xn) over the gathered rows: own rows + the peers' partials, the peers' rows sent
-  if ((rc = run_gemm("gemm_head_dx", s, tok, x.h, v_t, op(RowSrc::plain(dl, v_t), tok), Layout::KC,
-                     op(RowSrc::plain(w_lm, x.h), x.h), Layout::MN, epi_residual(x, dxn, nullptr, peer_dxn, send))))
-    return rc;
+  if (!split_k) {
+    if ((rc = run_gemm("gemm_head_dx", s, tok, x.h, v_t, op(RowSrc::plain(dl, v_t), tok), Layout::KC,
+                       op(RowSrc::plain(w_lm, x.h), x.h), Layout::MN, epi_residual(x, dxn, nullptr, peer_dxn, send))))
+      return rc;
+  } else {   // as in lm_head_xent: the bulk of K on the BK = 64 kernel, the tail on the ragged one, in fp32
+    float* sum = reinterpret_cast<float*>(wsb + o_sum);
+    const int64_t k1 = v_t - v_t % 128, k2 = v_t - k1;
+    EpiParams ef{};
+    ef.kind = EpiKind::StoreF32;
+    ef.c = sum;
+    ef.ldc = x.h;
+    if ((rc = run_gemm("gemm_head_dx", s, tok, x.h, k1, op(RowSrc::plain(dl, v_t), tok), Layout::KC,
+                       op(RowSrc::plain(w_lm, x.h), x.h), Layout::MN, ef)))
+      return rc;
+    if ((rc = run_gemm("gemm_head_dx_tail", s, tok, x.h, k2, op(RowSrc::plain(dl + k1, v_t), tok), Layout::KC,
+                       op(RowSrc::plain(static_cast<const uint16_t*>(w_lm) + k1 * x.h, x.h), x.h), Layout::MN,
+                       epi_acc(sum, x.h))))
+      return rc;
+    if ((rc = launch("sp_finish", s, [&] {
+           return sp_finish(sum, (int32_t)x.h, tok, (int32_t)x.s_c, (int32_t)x.s_sp, (int32_t)x.tr, (int32_t)x.t,
+                            static_cast<const uint16_t*>(peer_dxn), dxn, static_cast<uint16_t*>(send), s);
+         })))
+      return rc;
+  }
   if ((rc = launch("rmsnorm_bwd", s, [&] {
          return rmsnorm_bwd(sptr(st, L4D_HEAD_X), static_cast<const uint16_t*>(w_norm), dxn, nullptr,
                             static_cast<uint16_t*>(dx), partial, npart, rows_sp, (int32_t)x.h, x.eps, s);

@@ -219,6 +219,11 @@ hipError_t xent_grad(const float* probs, int64_t n, int32_t v_t, int64_t v0, con
 hipError_t embed_fwd(const int64_t* ids, const uint16_t* w, int64_t v0, int32_t v_t, int32_t h, int64_t rows,
                      int32_t s_c, int32_t s_sp, int32_t r, int32_t t, const uint16_t* receipt, uint16_t* own,
                      uint16_t* send, hipStream_t stream);
+// Rows of an fp32 [rows][h] sum over the gathered view: own SP rows ->
+// bf16(sum + receipt) into own (receipt may be null), the peers' rows ->
+// bf16(sum) into send (row mapping as RowSrc).
+hipError_t sp_finish(const float* sum, int32_t h, int64_t rows, int32_t s_c, int32_t s_sp, int32_t r, int32_t t,
+                     const uint16_t* receipt, uint16_t* own, uint16_t* send, hipStream_t stream);
 // dw[ids[m] - v0] += dy.row(m) for the ids in range (fp32 atomics).
 hipError_t embed_bwd(const int64_t* ids, RowSrc dy, int64_t v0, int32_t v_t, int32_t h, int64_t rows, float* dw,
                      hipStream_t stream);

@@ -484,6 +484,34 @@ __global__ void __launch_bounds__(256) embed_fwd_kernel(const int64_t* __restric
   }
 }
 
+// One wave per gathered row of an fp32 sum: own rows -> bf16(sum + receipt),
+// the peers' rows -> bf16(sum) into send (the residual epilogue of a GEMM
+// whose K was summed in two parts).
+__global__ void __launch_bounds__(256) sp_finish_kernel(const float* __restrict__ sum, int32_t h, int64_t rows,
+                                                       SpRows sp, const uint16_t* __restrict__ receipt,
+                                                       uint16_t* __restrict__ own, uint16_t* __restrict__ send) {
+  const int lane = threadIdx.x & 63;
+  const int64_t m = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (m >= rows) return;
+  const uint32_t o = sp.map(m);
+  const bool mine = !(o & 0x80000000u);
+  const int64_t orow = o & 0x7fffffffu;
+  const float4* src = reinterpret_cast<const float4*>(sum + m * h);
+  u32x4* dst = reinterpret_cast<u32x4*>((mine ? own : send) + orow * h);
+  const u32x4* rc = (mine && receipt) ? reinterpret_cast<const u32x4*>(receipt + orow * h) : nullptr;
+  for (int c = lane; c < h / 8; c += 64) {
+    const float4 a = src[2 * c], b = src[2 * c + 1];
+    float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    if (rc) {
+      float r[8];
+      unpack8(rc[c], r);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] += r[e];
+    }
+    dst[c] = pack8(f);
+  }
+}
+
 // One wave per gathered row whose id is in range: dW[id - v0] += dY[row]
 // (fp32 atomic adds: rows that share an id add in no fixed order).
 __global__ void __launch_bounds__(256) embed_bwd_kernel(const int64_t* __restrict__ ids, RowSrc dy, int64_t v0,
@@ -583,6 +611,14 @@ hipError_t embed_fwd(const int64_t* ids, const uint16_t* w, int64_t v0, int32_t 
   if (rows <= 0) return hipSuccess;
   hipLaunchKernelGGL(embed_fwd_kernel, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, ids, w,
                      v0, v_t, h, rows, SpRows{s_c, s_sp, r, t}, receipt, own, send);
+  return hipGetLastError();
+}
+
+hipError_t sp_finish(const float* sum, int32_t h, int64_t rows, int32_t s_c, int32_t s_sp, int32_t r, int32_t t,
+                     const uint16_t* receipt, uint16_t* own, uint16_t* send, hipStream_t stream) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(sp_finish_kernel, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, sum, h, rows,
+                     SpRows{s_c, s_sp, r, t}, receipt, own, send);
   return hipGetLastError();
 }
 

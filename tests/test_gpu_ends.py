@@ -23,7 +23,7 @@ from gpu_common import check, dev_bf16, host_f64
 
 pytestmark = pytest.mark.gpu
 
-CASES = [W.ENDS_TINY, W.ENDS_TP2CP2_RAGGED, W.ENDS_MID]
+CASES = [W.ENDS_TINY, W.ENDS_TP2CP2_RAGGED, W.ENDS_MID, W.ENDS_RAGGED_VOCAB]
 
 
 def shard_of(w):

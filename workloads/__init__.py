@@ -341,5 +341,7 @@ ENDS_TINY = EndsWorkload("ends-tiny", 256, 4, 2, 688, 1024, 128)
 ENDS_TP2CP2_RAGGED = EndsWorkload("ends-tp2cp2-ragged", 512, 4, 2, 1376, 2000, 400, micro_batch=2, tp=2, cp=2,
                                   tp_rank=1, cp_rank=1)
 ENDS_MID = EndsWorkload("ends-mid-tp2", 1024, 8, 8, 2816, 8192, 1024, tp=2, tp_rank=0)
+# a vocabulary shard of 1288 (not a multiple of 128): d(xn) is summed over two GEMM kernels
+ENDS_RAGGED_VOCAB = EndsWorkload("ends-tp2-vocab1288", 512, 4, 2, 1376, 2576, 256, tp=2, tp_rank=1)
 # The Llama-3-8B head at TP4 (8192 tokens, vocabulary shard 32064 of 128256).
 ENDS_LLAMA3_8B_TP4 = EndsWorkload("ends-llama3-8b-tp4", 4096, 32, 8, 14336, 128256, 8192, tp=4, tp_rank=1)
