@@ -35,8 +35,6 @@
 // LDS and hands 8-column vectors to the fused operation, with that operation's
 // global inputs loaded for a whole pass first.  The fp32 accumulate (dW) needs
 // no staging: the accumulators start from the C tile and are stored back.
-#include <stdlib.h>
-
 #include "kernels.h"
 
 namespace l4d {
@@ -961,19 +959,11 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   }
 }
 
-// Kernel choice: K a multiple of 128 takes the 8-wave BK = 64 kernel (the
-// fastest of the three on the Llama layer shapes), any other K the BK = 32
-// kernel.  L4D_GEMM_VARIANT = 32 | 64 (4-wave BK = 64) | 68 forces one.
-int gemm_variant_env() {
-  static int v = [] {
-    const char* e = getenv("L4D_GEMM_VARIANT");
-    return e ? atoi(e) : 0;
-  }();
-  return v;
-}
-
+// Kernel choice: K a multiple of 128 (and every K split) takes the 8-wave
+// BK = 64 kernel, the fastest on the Llama layer shapes; any other K the
+// BK = 32 kernel, whose copies mask the ragged end of K.
 template <Layout LA, Layout LB, EpiKind KIND, int PAIR>
-hipError_t launch(const GemmParams& p, hipStream_t stream, int variant) {
+hipError_t launch(const GemmParams& p, hipStream_t stream) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = p.B.split_rows ? (p.B.split_rows + 127) / 128 : (p.N + BN - 1) / BN;
   const int parts = p.k_splits > 1 ? p.k_splits : 1;
@@ -981,17 +971,7 @@ hipError_t launch(const GemmParams& p, hipStream_t stream, int variant) {
                     !p.partial))
     return hipErrorInvalidValue;
   const dim3 grid(tiles_m * tiles_n * parts);
-  if (variant == 0) variant = gemm_variant_env();
-  if (variant == 0) variant = 68;
-  if (p.K % (2 * BK2) != 0) variant = 32;
-  if (parts > 1) variant = 68;
-  if constexpr (LA == Layout::MN) {
-    if (variant == 64) variant = 68;     // the 4-wave kernel needs stack space with two MN operands
-  }
-  if (variant == 64) {
-    if constexpr (LA != Layout::MN)
-      hipLaunchKernelGGL((gemm_bk64<LA, LB, KIND, PAIR, 4>), grid, dim3(256), 0, stream, p);
-  } else if (variant == 68)
+  if (p.K % (2 * BK2) == 0)
     hipLaunchKernelGGL((gemm_bk64<LA, LB, KIND, PAIR, 8>), grid, dim3(512), 0, stream, p);
   else
     hipLaunchKernelGGL((gemm_bk32<LA, LB, KIND, PAIR>), grid, dim3(512), 0, stream, p);
@@ -1000,32 +980,26 @@ hipError_t launch(const GemmParams& p, hipStream_t stream, int variant) {
 
 }  // namespace
 
-hipError_t gemm_variant(const GemmParams& p, Layout la, Layout lb, hipStream_t stream, int variant);
-
 hipError_t gemm(const GemmParams& p, Layout la, Layout lb, hipStream_t stream) {
-  return gemm_variant(p, la, lb, stream, 0);
-}
-
-hipError_t gemm_variant(const GemmParams& p, Layout la, Layout lb, hipStream_t stream, int variant) {
   if (p.M <= 0 || p.N <= 0 || p.K <= 0) return hipSuccess;
   using L = Layout;
   using E = EpiKind;
   const E k = p.epi.kind;
   if (la == L::KC && lb == L::KC) {
-    if (k == E::QkvRope && p.epi.d_h == 128) return launch<L::KC, L::KC, E::QkvRope, 64>(p, stream, variant);
-    if (k == E::QkvRope && p.epi.d_h == 64) return launch<L::KC, L::KC, E::QkvRope, 32>(p, stream, variant);
-    if (k == E::ResidualSP) return launch<L::KC, L::KC, E::ResidualSP, 128>(p, stream, variant);
-    if (k == E::SwiGLUFwd) return launch<L::KC, L::KC, E::SwiGLUFwd, 128>(p, stream, variant);
-    if (k == E::StoreBF16) return launch<L::KC, L::KC, E::StoreBF16, 128>(p, stream, variant);
-    if (k == E::StoreF32) return launch<L::KC, L::KC, E::StoreF32, 128>(p, stream, variant);
+    if (k == E::QkvRope && p.epi.d_h == 128) return launch<L::KC, L::KC, E::QkvRope, 64>(p, stream);
+    if (k == E::QkvRope && p.epi.d_h == 64) return launch<L::KC, L::KC, E::QkvRope, 32>(p, stream);
+    if (k == E::ResidualSP) return launch<L::KC, L::KC, E::ResidualSP, 128>(p, stream);
+    if (k == E::SwiGLUFwd) return launch<L::KC, L::KC, E::SwiGLUFwd, 128>(p, stream);
+    if (k == E::StoreBF16) return launch<L::KC, L::KC, E::StoreBF16, 128>(p, stream);
+    if (k == E::StoreF32) return launch<L::KC, L::KC, E::StoreF32, 128>(p, stream);
   } else if (la == L::KC && lb == L::MN) {
-    if (k == E::SwiGLUBwd) return launch<L::KC, L::MN, E::SwiGLUBwd, 128>(p, stream, variant);
-    if (k == E::ResidualSP) return launch<L::KC, L::MN, E::ResidualSP, 128>(p, stream, variant);
-    if (k == E::StoreBF16) return launch<L::KC, L::MN, E::StoreBF16, 128>(p, stream, variant);
-    if (k == E::StoreF32) return launch<L::KC, L::MN, E::StoreF32, 128>(p, stream, variant);
-    if (k == E::AccF32) return launch<L::KC, L::MN, E::AccF32, 128>(p, stream, variant);
+    if (k == E::SwiGLUBwd) return launch<L::KC, L::MN, E::SwiGLUBwd, 128>(p, stream);
+    if (k == E::ResidualSP) return launch<L::KC, L::MN, E::ResidualSP, 128>(p, stream);
+    if (k == E::StoreBF16) return launch<L::KC, L::MN, E::StoreBF16, 128>(p, stream);
+    if (k == E::StoreF32) return launch<L::KC, L::MN, E::StoreF32, 128>(p, stream);
+    if (k == E::AccF32) return launch<L::KC, L::MN, E::AccF32, 128>(p, stream);
   } else if (la == L::MN && lb == L::MN) {
-    if (k == E::AccF32) return launch<L::MN, L::MN, E::AccF32, 128>(p, stream, variant);
+    if (k == E::AccF32) return launch<L::MN, L::MN, E::AccF32, 128>(p, stream);
   }
   return hipErrorInvalidValue;     // a layout / epilogue pairing the layer never uses
 }
