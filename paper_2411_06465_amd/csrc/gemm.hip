@@ -484,10 +484,10 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, f32x16 (&acc)[4]
 // is loaded into them before the first product (its latency overlaps the first
 // stage's copies) and stored from them at the end.  In the accumulator layout
 // the 32 lanes of a half-wave cover 32 consecutive columns (128 bytes) of one
-// row, so both are whole-line accesses without staging.  The store is
-// non-temporal: the tile is not read again in this launch, and streaming it
-// leaves L2 to the operand tiles the neighbouring workgroups share (3% off the
-// largest weight-gradient GEMM of the Llama-2-7B layer).
+// row, so both are whole-line accesses without staging.  Whole tiles load and
+// store non-temporally: each C element is touched once per launch, and
+// streaming it leaves L2 to the operand tiles the neighbouring workgroups share
+// (4-5% off the largest weight-gradient GEMM of the Llama-2-7B layer).
 template <int NS>
 __device__ __forceinline__ void acc_load_f32(f32x16 (&acc)[4][NS], const GemmParams& p, const float* cbase,
                                              int64_t ldc, int64_t row0, int tn, const int* ncol, int lane) {
@@ -496,22 +496,30 @@ __device__ __forceinline__ void acc_load_f32(f32x16 (&acc)[4][NS], const GemmPar
 #pragma unroll
   for (int ns = 0; ns < NS; ++ns) off[ns] = static_cast<int32_t>(rl * ldc) + tn * BN + ncol[ns] + (lane & 31);
   const bool full = row0 + 128 <= p.M && (tn + 1) * BN <= p.N;   // uniform
+  if (full) {
 #pragma unroll
-  for (int ms = 0; ms < 4; ++ms)
+    for (int ms = 0; ms < 4; ++ms)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int r = ms * 32 + 8 * (i >> 2) + (i & 3);
-      const float* row = cbase + (row0 + r) * ldc;   // uniform
+      for (int i = 0; i < 16; ++i) {
+        const int r = ms * 32 + 8 * (i >> 2) + (i & 3);
+        const float* row = cbase + (row0 + r) * ldc;   // uniform
 #pragma unroll
-      for (int ns = 0; ns < NS; ++ns) {
-        if (full) {
-          acc[ms][ns][i] = row[off[ns]];
-        } else {
+        for (int ns = 0; ns < NS; ++ns) acc[ms][ns][i] = __builtin_nontemporal_load(&row[off[ns]]);
+      }
+  } else {
+#pragma unroll
+    for (int ms = 0; ms < 4; ++ms)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = ms * 32 + 8 * (i >> 2) + (i & 3);
+        const float* row = cbase + (row0 + r) * ldc;   // uniform
+#pragma unroll
+        for (int ns = 0; ns < NS; ++ns) {
           const int n = tn * BN + ncol[ns] + (lane & 31);
           acc[ms][ns][i] = (row0 + r + rl < p.M && n < p.N) ? row[off[ns]] : 0.0f;
         }
       }
-    }
+  }
 }
 
 template <int NS>
