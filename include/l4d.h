@@ -371,6 +371,10 @@ int l4d_profile_read(const char* name, int64_t* launches, double* total_ms);
 /* Newline-separated "name launches total_ms" lines into buf (truncated to
  * buf_len); returns the needed length through *needed. */
 int l4d_profile_dump(char* buf, uint64_t buf_len, uint64_t* needed);
+/* The labels of the timed launches since the last reset, newline-separated,
+ * in launch order (e.g. to label the dispatches of an external kernel trace);
+ * same buffer convention as l4d_profile_dump. */
+int l4d_profile_order(char* buf, uint64_t buf_len, uint64_t* needed);
 int l4d_profile_reset(void);
 
 #ifdef __cplusplus

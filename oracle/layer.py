@@ -38,9 +38,12 @@ Readings of points the paper leaves open:
   * SwiGLU: act = silu(G), prod = act * U; the stash keeps G, U, act, prod.
   * storage: every tensor the layer stores is bf16 (Sec. 3.2 counts 2 bytes
     per activation); each stored tensor is computed from the stored values of
-    its inputs and rounded once.  Weight and norm-gain gradients are float32
-    accumulators in the library (Sec. 3.1: gradients accumulate in FP32) and
-    are returned here in float64.
+    its inputs and rounded once.  In the backward, the gradients that are the
+    operands of products (dG|dU, dh1, d ctx, dQ|dK|dV) are stored in bf16 as
+    well; d(xn2), d(xn1) and the copy of dh1 that dx adds are kept in fp32
+    (they feed only the RMSNorm backward), so they are not rounded here.
+    Weight and norm-gain gradients are float32 accumulators in the library
+    (Sec. 3.1: gradients accumulate in FP32) and are returned here in float64.
 """
 import numpy as np
 
@@ -265,10 +268,11 @@ def layer_backward(sh, w, st, dy, peers=None, exact=False):
     dxn2_own, dxn2_peer = split_own(sh, dgu @ w["gate_up"])
     if peers.get("sp_peer_dxn2") is not None:
         dxn2_own = dxn2_own + peers["sp_peer_dxn2"]
-    dxn2 = rnd(dxn2_own)
+    dxn2 = dxn2_own                             # kept in fp32: feeds only the norm backward
     out["dxn2_send"] = rnd(dxn2_peer)
     dh1_n, out["d_norm2"] = rmsnorm_bwd(st["h1"], w["norm2"], sh.eps, dxn2)
-    dh1 = rnd(dy + dh1_n)
+    dh1_res = dy + dh1_n                        # fp32: the residual added into dx
+    dh1 = rnd(dh1_res)                          # bf16: operand of the O-projection products
 
     # attention block: h1 = x + ctx W_O^T
     dh1_full = gather(sh, dh1, peers.get("sp_peer_dh1"))
@@ -297,104 +301,10 @@ def layer_backward(sh, w, st, dy, peers=None, exact=False):
     dxn1_own, dxn1_peer = split_own(sh, dqkv @ w["qkv"])
     if peers.get("sp_peer_dxn1") is not None:
         dxn1_own = dxn1_own + peers["sp_peer_dxn1"]
-    dxn1 = rnd(dxn1_own)
+    dxn1 = dxn1_own                             # kept in fp32: feeds only the norm backward
     out["dxn1_send"] = rnd(dxn1_peer)
     dx_n, out["d_norm1"] = rmsnorm_bwd(st["x"], w["norm1"], sh.eps, dxn1)
-    out["dx"] = rnd(dh1 + dx_n)
+    out["dx"] = rnd(dh1_res + dx_n)
     # intermediates, for localising a mismatch
     out.update(dgu=dgu, dxn2=dxn2, dh1=dh1, dctx=dctx, dqkv=dqkv, dxn1=dxn1)
     return out
-
-
-# ---------------------------------------------------------------- sampled rows
-# The same layer evaluated at a few rows only, for checks at full model size
-# where the full oracle would take too long.  Nothing here is new arithmetic:
-# each quantity is the one above restricted to the rows asked for, with the
-# same rounding points.
-
-def layer_forward_rows(sh, w, x, rows, peers=None):
-    """Forward outputs at the own rows ``rows`` (indices into [0, s_sp)).
-    K and V are computed for every local token (every query may see them);
-    everything else only for the rows asked for.  Returns y, x, xn1, h1, xn2 at
-    those own rows, q, k, v, ctx, gate, up, act, prod at the matching local
-    tokens, and lse [b, a_t, len(rows)]."""
-    peers = peers or {}
-    rows = np.asarray(rows)
-    pos, rpos = sh.positions()
-    d = sh.d_h
-    nq, nk = sh.a_t * d, sh.k_t * d
-    m = sh.tp_rank * sh.s_sp + rows                     # local token index of each own row
-
-    xn1_own = round_bf16(rmsnorm(x, w["norm1"], sh.eps))
-    xn1_full = gather(sh, xn1_own, peers.get("sp_peer_xn1"))
-    kv = xn1_full @ w["qkv"][nq:].T
-    k = round_bf16(rope(kv[..., :nk], pos, d, sh.base))
-    v = round_bf16(kv[..., nk:])
-    q = round_bf16(rope(xn1_full[:, m] @ w["qkv"][:nq].T, pos[m], d, sh.base))
-    k_all, v_all, k_pos = k, v, pos
-    if sh.c > 1:
-        k_all = np.concatenate([k, peers["remote_k"]], axis=1)
-        v_all = np.concatenate([v, peers["remote_v"]], axis=1)
-        k_pos = np.concatenate([pos, rpos])
-    ctx_f, lse = attention(sh, q, k_all, v_all, pos[m], k_pos)
-    ctx = round_bf16(ctx_f)
-
-    h1 = x[:, rows] + ctx @ w["o"].T
-    if peers.get("sp_peer_o") is not None:
-        h1 = h1 + peers["sp_peer_o"][:, rows]
-    h1 = round_bf16(h1)
-    xn2 = round_bf16(rmsnorm(h1, w["norm2"], sh.eps))
-    gu = xn2 @ w["gate_up"].T
-    gate, up = round_bf16(gu[..., :sh.f_t]), round_bf16(gu[..., sh.f_t:])
-    a = silu(gate)
-    act, prod = round_bf16(a), round_bf16(a * up)
-    y = h1 + prod @ w["down"].T
-    if peers.get("sp_peer_ffn") is not None:
-        y = y + peers["sp_peer_ffn"][:, rows]
-    y = round_bf16(y)
-    return dict(y=y, x=x[:, rows], xn1=xn1_own[:, rows], q=q, k=k[:, m], v=v[:, m], ctx=ctx, h1=h1, xn2=xn2,
-                gate=gate, up=up, act=act, prod=prod, lse=lse)
-
-
-def layer_backward_last_rows(sh, w, x, dy, n_last, peers=None):
-    """dx at the last ``n_last`` local rows of a shard without tensor
-    parallelism (t = 1).  Those rows hold the largest positions of the rank,
-    so every local query that sees one of their keys is itself among them:
-    their dK/dV need no other local row (the other CP ranks' share arrives as
-    cp_peer_dk/dv).  Returns dx [b, n_last, h]."""
-    assert sh.t == 1
-    peers = peers or {}
-    pos, rpos = sh.positions()
-    d = sh.d_h
-    nq, nk = sh.a_t * d, sh.k_t * d
-    rows = np.arange(sh.s_c - n_last, sh.s_c)
-    f = layer_forward_rows(sh, w, x, rows, peers)
-    xn1_full = round_bf16(rmsnorm(x, w["norm1"], sh.eps))
-    kv = xn1_full @ w["qkv"][nq:].T
-    k = round_bf16(rope(kv[..., :nk], pos, d, sh.base))
-    v = round_bf16(kv[..., nk:])
-    k_all, v_all, k_pos = k, v, pos
-    if sh.c > 1:
-        k_all = np.concatenate([k, peers["remote_k"]], axis=1)
-        v_all = np.concatenate([v, peers["remote_v"]], axis=1)
-        k_pos = np.concatenate([pos, rpos])
-
-    dyr = dy[:, rows]
-    dprod = dyr @ w["down"]
-    sg = 1.0 / (1.0 + np.exp(-f["gate"]))
-    dgate = dprod * f["up"] * (sg * (1.0 + f["gate"] * (1.0 - sg)))
-    dup = dprod * f["act"]
-    dgu = round_bf16(np.concatenate([dgate, dup], axis=-1))
-    dxn2 = round_bf16(dgu @ w["gate_up"])
-    dh1 = round_bf16(dyr + rmsnorm_bwd(f["h1"], w["norm2"], sh.eps, dxn2)[0])
-    dctx = round_bf16(dh1 @ w["o"])
-    dq, dk_all, dv_all = attention_bwd(sh, f["q"], k_all, v_all, pos[rows], k_pos, dctx)
-    dk_loc, dv_loc = dk_all[:, rows], dv_all[:, rows]
-    if peers.get("cp_peer_dk") is not None:
-        dk_loc = dk_loc + peers["cp_peer_dk"][:, rows]
-        dv_loc = dv_loc + peers["cp_peer_dv"][:, rows]
-    dq = round_bf16(rope(dq, pos[rows], d, sh.base, inverse=True))
-    dk = round_bf16(rope(dk_loc, pos[rows], d, sh.base, inverse=True))
-    dv = round_bf16(dv_loc)
-    dxn1 = round_bf16(np.concatenate([dq, dk, dv], axis=-1) @ w["qkv"])
-    return round_bf16(dh1 + rmsnorm_bwd(x[:, rows], w["norm1"], sh.eps, dxn1)[0])

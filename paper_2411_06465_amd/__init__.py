@@ -107,6 +107,7 @@ def lib():
             "l4d_profile_only": ([C.c_char_p], C.c_int),
             "l4d_profile_read": ([C.c_char_p, C.POINTER(i64), C.POINTER(C.c_double)], C.c_int),
             "l4d_profile_dump": ([C.c_char_p, u64, C.POINTER(u64)], C.c_int),
+            "l4d_profile_order": ([C.c_char_p, u64, C.POINTER(u64)], C.c_int),
             "l4d_profile_reset": ([], C.c_int),
         }
         for name, (args, res) in sig.items():
@@ -349,3 +350,12 @@ def l4d_profile_dump():
         name, cnt, ms = line.split()
         out[name] = (int(cnt), float(ms))
     return out
+
+
+def l4d_profile_order():
+    """Labels of the timed launches since the last reset, in launch order."""
+    need = C.c_uint64()
+    _check(lib().l4d_profile_order(None, 0, C.byref(need)))
+    buf = C.create_string_buffer(need.value + 1)
+    _check(lib().l4d_profile_order(buf, need.value + 1, C.byref(need)))
+    return buf.value.decode().split()

@@ -54,6 +54,7 @@ std::string g_prof_only;            // non-empty: time only the launches with th
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_event_pool;
 std::map<std::string, std::pair<int64_t, double>> g_totals;
+std::vector<const char*> g_order;  // labels of the timed launches since the last reset, in launch order
 
 hipEvent_t take_event() {
   if (!g_event_pool.empty()) {
@@ -73,6 +74,7 @@ int drain_pending() {
     if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.a, p.b);
     if (e != hipSuccess) return fail(L4D_EDEVICE, "profile events: %s", hipGetErrorString(e));
     auto& t = g_totals[p.name];
+    g_order.push_back(p.name);
     t.first += 1;
     t.second += ms;
     g_event_pool.push_back(p.a);
@@ -119,6 +121,7 @@ extern "C" int l4d_profile_reset(void) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   int rc = drain_pending();
   g_totals.clear();
+  g_order.clear();
   return rc;
 }
 
@@ -147,6 +150,24 @@ extern "C" int l4d_profile_dump(char* buf, uint64_t buf_len, uint64_t* needed) {
   for (auto& kv : g_totals) {
     snprintf(line, sizeof line, "%s %lld %.6f\n", kv.first.c_str(), (long long)kv.second.first, kv.second.second);
     out += line;
+  }
+  if (needed) *needed = out.size() + 1;
+  if (buf && buf_len) {
+    size_t n = std::min<size_t>(out.size(), buf_len - 1);
+    memcpy(buf, out.data(), n);
+    buf[n] = 0;
+  }
+  return L4D_OK;
+}
+
+extern "C" int l4d_profile_order(char* buf, uint64_t buf_len, uint64_t* needed) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  int rc = drain_pending();
+  if (rc) return rc;
+  std::string out;
+  for (const char* n : g_order) {
+    out += n;
+    out += '\n';
   }
   if (needed) *needed = out.size() + 1;
   if (buf && buf_len) {
@@ -488,7 +509,7 @@ struct FwdWs {
   uint64_t rope, o_send, ffn_send, total;
 };
 struct BwdWs {
-  uint64_t rope, dgu, dxn2, dh1, dctx, delta, dqkv, dxn1, partial, dxn2_send, dxn1_send, dkv, dwpart, total;
+  uint64_t rope, dgu, dxn2, dh1, dh1_f32, dctx, delta, dqkv, dxn1, partial, dxn2_send, dxn1_send, dkv, dwpart, total;
 };
 
 uint64_t split_ws_bytes(int64_t M, int64_t N, int64_t K, bool acc_f32 = true) {
@@ -514,12 +535,13 @@ BwdWs plan_bwd(const Shard& x, const l4d_peer_outputs* sends) {
   const uint64_t peer_rows = x.b * (x.t - 1) * x.s_sp * x.h * 2;
   w.rope = cv.take(x.s_c * (x.d / 2) * 8);
   w.dgu = cv.take(tok * 2 * x.f_t * 2);
-  w.dxn2 = cv.take(sp);
-  w.dh1 = cv.take(sp);
+  w.dxn2 = cv.take(2 * sp);       // fp32: only the norm backward reads it
+  w.dh1 = cv.take(sp);            // bf16: operand of the output-projection products
+  w.dh1_f32 = cv.take(2 * sp);    // fp32: the residual the norm-1 backward adds
   w.dctx = cv.take(tok * x.a_t * x.d * 2);
   w.delta = cv.take(x.b * x.a_t * x.s_c * 4);
   w.dqkv = cv.take(tok * qkv_cols(x) * 2);
-  w.dxn1 = cv.take(sp);
+  w.dxn1 = cv.take(2 * sp);       // fp32
   w.partial = cv.take((uint64_t)rmsnorm_bwd_partials(x.b * x.s_sp) * x.h * 4);
   w.dxn2_send = (x.t > 1 && !(sends && sends->dxn2_partial)) ? cv.take(peer_rows) : 0;
   w.dxn1_send = (x.t > 1 && !(sends && sends->dxn1_partial)) ? cv.take(peer_rows) : 0;
@@ -581,11 +603,12 @@ inline RowSrc gathered(const void* own, const void* peer, const Shard& x) {
 inline Operand op(RowSrc src, int64_t rows) { return Operand{src, (int32_t)rows, 0, 0}; }
 
 inline EpiParams epi_residual(const Shard& x, uint16_t* own_out, const void* resid, const void* receipt,
-                              void* send) {
+                              void* send, float* own_out_f32 = nullptr) {
   EpiParams e{};
   e.kind = EpiKind::ResidualSP;
   e.ldc = x.h;
   e.own_out = own_out;
+  e.own_out_f32 = own_out_f32;
   e.resid = static_cast<const uint16_t*>(resid);
   e.receipt = static_cast<const uint16_t*>(receipt);
   e.send = static_cast<uint16_t*>(send);
@@ -850,8 +873,9 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
   uint8_t* wsb = reinterpret_cast<uint8_t*>(A->base + ws.off);
   auto W = [&](uint64_t off) { return reinterpret_cast<uint16_t*>(wsb + off); };
   float2* rope = reinterpret_cast<float2*>(wsb + plan.rope);
-  uint16_t *dgu = W(plan.dgu), *dxn2 = W(plan.dxn2), *dh1 = W(plan.dh1), *dctx = W(plan.dctx);
-  uint16_t *dqkv = W(plan.dqkv), *dxn1 = W(plan.dxn1);
+  uint16_t *dgu = W(plan.dgu), *dh1 = W(plan.dh1), *dctx = W(plan.dctx), *dqkv = W(plan.dqkv);
+  auto F = [&](uint64_t off) { return reinterpret_cast<float*>(wsb + off); };
+  float *dxn2 = F(plan.dxn2), *dxn1 = F(plan.dxn1), *dh1_f32 = F(plan.dh1_f32);
   float* delta = reinterpret_cast<float*>(wsb + plan.delta);
   float* partial = reinterpret_cast<float*>(wsb + plan.partial);
   float* dwpart = plan.dwpart ? reinterpret_cast<float*>(wsb + plan.dwpart) : nullptr;
@@ -885,16 +909,17 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
     // d(xn2) = dGU W_gu (own rows + receipt; peers' rows sent)
     if ((r = run_gemm("gemm_gate_up_dx", s, tok, x.h, 2 * x.f_t, op(RowSrc::plain(dgu, 2 * x.f_t), tok), Layout::KC,
                       op(RowSrc::plain(w->gate_up, x.h), x.h), Layout::MN,
-                      epi_residual(x, dxn2, nullptr, pi.sp_peer_dxn2, dxn2_send))))
+                      epi_residual(x, nullptr, nullptr, pi.sp_peer_dxn2, dxn2_send, dxn2))))
       return r;
     const RowSrc xn2_full = gathered(sptr(st, L4D_STASH_XN2), pi.sp_peer_xn2, x);
     if ((r = run_gemm("gemm_gate_up_dw", s, 2 * x.f_t, x.h, tok, op(RowSrc::plain(dgu, 2 * x.f_t), 2 * x.f_t),
                       Layout::MN, op(xn2_full, x.h), Layout::MN, epi_acc(dw->gate_up, x.h), dwpart)))
       return r;
-    // norm-2 backward + residual
+    // norm-2 backward + residual: dh1 in bf16 (product operand) and fp32 (residual of dx)
     if ((r = launch("rmsnorm_bwd", s, [&] {
-           return rmsnorm_bwd(sptr(st, L4D_STASH_H1), static_cast<const uint16_t*>(w->norm2), dxn2,
-                              static_cast<const uint16_t*>(dy), dh1, partial, npart, rows_sp, (int32_t)x.h, x.eps, s);
+           const NormBwdIo io{nullptr, dxn2, static_cast<const uint16_t*>(dy), nullptr, dh1, dh1_f32};
+           return rmsnorm_bwd(sptr(st, L4D_STASH_H1), static_cast<const uint16_t*>(w->norm2), io, partial, npart,
+                              rows_sp, (int32_t)x.h, x.eps, s);
          })))
       return r;
     if ((r = launch("reduce_gain", s, [&] { return reduce_rows_add(partial, npart, (int32_t)x.h, dw->norm2, s); })))
@@ -937,7 +962,7 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
     // QKV projection
     if ((r = run_gemm("gemm_qkv_dx", s, tok, x.h, qc, op(RowSrc::plain(dqkv, qc), tok), Layout::KC,
                       op(RowSrc::plain(w->qkv, x.h), x.h), Layout::MN,
-                      epi_residual(x, dxn1, nullptr, pi.sp_peer_dxn1, dxn1_send))))
+                      epi_residual(x, nullptr, nullptr, pi.sp_peer_dxn1, dxn1_send, dxn1))))
       return r;
     const RowSrc xn1_full = gathered(sptr(st, L4D_STASH_XN1), pi.sp_peer_xn1, x);
     if ((r = run_gemm("gemm_qkv_dw", s, qc, x.h, tok, op(RowSrc::plain(dqkv, qc), qc), Layout::MN, op(xn1_full, x.h),
@@ -945,8 +970,9 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
       return r;
     // norm-1 backward + residual
     if ((r = launch("rmsnorm_bwd", s, [&] {
-           return rmsnorm_bwd(sptr(st, L4D_STASH_X), static_cast<const uint16_t*>(w->norm1), dxn1, dh1,
-                              static_cast<uint16_t*>(dx), partial, npart, rows_sp, (int32_t)x.h, x.eps, s);
+           const NormBwdIo io{nullptr, dxn1, nullptr, dh1_f32, static_cast<uint16_t*>(dx), nullptr};
+           return rmsnorm_bwd(sptr(st, L4D_STASH_X), static_cast<const uint16_t*>(w->norm1), io, partial, npart,
+                              rows_sp, (int32_t)x.h, x.eps, s);
          })))
       return r;
     if ((r = launch("reduce_gain", s, [&] { return reduce_rows_add(partial, npart, (int32_t)x.h, dw->norm1, s); })))
@@ -1193,8 +1219,9 @@ extern "C" int lm_head_bwd(const l4d_model* m, const l4d_parallel* p, const void
       return rc;
   }
   if ((rc = launch("rmsnorm_bwd", s, [&] {
-         return rmsnorm_bwd(sptr(st, L4D_HEAD_X), static_cast<const uint16_t*>(w_norm), dxn, nullptr,
-                            static_cast<uint16_t*>(dx), partial, npart, rows_sp, (int32_t)x.h, x.eps, s);
+         const NormBwdIo io{dxn, nullptr, nullptr, nullptr, static_cast<uint16_t*>(dx), nullptr};
+         return rmsnorm_bwd(sptr(st, L4D_HEAD_X), static_cast<const uint16_t*>(w_norm), io, partial, npart,
+                            rows_sp, (int32_t)x.h, x.eps, s);
        })))
     return rc;
   if ((rc = launch("reduce_gain", s, [&] { return reduce_rows_add(partial, npart, (int32_t)x.h, d_w_norm, s); })))

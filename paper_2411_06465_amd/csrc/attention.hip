@@ -200,6 +200,15 @@ __device__ __forceinline__ bf16x8 frag_acc(const f32x16& s, int i0) {
   return __builtin_bit_cast(bf16x8, u32x4{pack2(s[i0], s[i0 + 1]), pack2(s[i0 + 2], s[i0 + 3]),
                                           pack2(s[i0 + 4], s[i0 + 5]), pack2(s[i0 + 6], s[i0 + 7])});
 }
+// The rounding residual of frag_acc: bf16(s - hi) for the same 8 registers,
+// given hi = frag_acc(s, i0).  hi + lo carries about 16 significant bits.
+__device__ __forceinline__ bf16x8 frag_acc_lo(const f32x16& s, int i0, bf16x8 hi) {
+  const u32x4 h = __builtin_bit_cast(u32x4, hi);
+  u32x4 r;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) r[k] = pack2(s[i0 + 2 * k] - lo16(h[k]), s[i0 + 2 * k + 1] - hi16(h[k]));
+  return __builtin_bit_cast(bf16x8, r);
+}
 // Row of accumulator register i for this lane (32x32 MFMA output layout).
 __device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 
@@ -306,6 +315,80 @@ __device__ __forceinline__ void run_ring2(const AttnParams& p, int pos_max, int 
   }
 }
 
+// ------------------------------------------------------------------ pipelined products
+// Two accumulator chains over the D columns of LDS tiles, with the B operands
+// in registers:  s0 += A0[r0 + (0..31)] x0^T,  s1 += A1[r1 + (0..31)] x1^T.
+// The schedule keeps LA fragment reads in flight ahead of the products
+// (without it the compiler reads each fragment right before its product and
+// the LDS latency is exposed on every step).
+template <int D, int LA>
+__device__ __forceinline__ void scores2(const uint8_t* a0, int r0, const bf16x8 (&x0)[D / 16], f32x16& s0,
+                                        const uint8_t* a1, int r1, const bf16x8 (&x1)[D / 16], f32x16& s1,
+                                        LaneAddr la) {
+  constexpr int N = D / 8;               // products (and fragment reads)
+  constexpr int L = LA < N ? LA : N - 1;
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) {
+    s0 = mfma(frag_rows<D>(a0, r0, kk, la), x0[kk], s0);
+    s1 = mfma(frag_rows<D>(a1, r1, kk, la), x1[kk], s1);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x100, L, 0);      // LDS reads
+#pragma unroll
+  for (int i = 0; i < N - L; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, L, 0);
+}
+
+// acc[dt] += A^T x over NG groups of 16 rows: A the LDS tile read transposed
+// (d rows, row-index contraction), x[g] a bf16 operand from registers (P^T,
+// dS^T); two reads per fragment, LA fragments in flight.
+template <int D, int NG, int LA>
+__device__ __forceinline__ void accum_t(const uint8_t* lds, const bf16x8 (&x)[NG], f32x16 (&acc)[D / 32], LaneAddr la) {
+  constexpr int N = NG * D / 32;
+  constexpr int L = LA < N ? LA : N - 1;
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) acc[dt] = mfma(frag_cols<D>(lds, dt, g, la), x[g], acc[dt]);
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * L, 0);
+#pragma unroll
+  for (int i = 0; i < N - L; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, L, 0);
+}
+
+// acc[dt] += A^T (xh + xl): as accum_t with the register operand split into a
+// high and a low bf16 part; each transposed fragment feeds both products, and
+// the high products of a group's column blocks go before their low products,
+// so no product waits on the one just before it.
+template <int D, int NG, int LA>
+__device__ __forceinline__ void accum_t2(const uint8_t* lds, const bf16x8 (&xh)[NG], const bf16x8 (&xl)[NG],
+                                         f32x16 (&acc)[D / 32], LaneAddr la) {
+  constexpr int N = NG * D / 32;
+  constexpr int L = LA < N ? LA : N - 1;
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    bf16x8 f[D / 32];
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) f[dt] = frag_cols<D>(lds, dt, g, la);
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) acc[dt] = mfma(f[dt], xh[g], acc[dt]);
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) acc[dt] = mfma(f[dt], xl[g], acc[dt]);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * L, 0);
+#pragma unroll
+  for (int i = 0; i < N - L; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 2 * L, 0);
+}
+
 template <int D>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) attn_fwd_kernel(AttnParams p) {
   constexpr int TB = KT * D * 2;
@@ -385,10 +468,16 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))
         rs += pr;
       }
     l_run += rs;
-    bf16x8 pf[4];
+    // P enters the P V product as bf16 hi + lo parts (two products per V
+    // fragment): a plain bf16 P carries a relative error of up to 2^-9 into
+    // every output, which the bf16 stores after attention then amplify.
+    bf16x8 pf[4], pl[4];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) pf[g] = frag_acc(sc[g >> 1], 8 * (g & 1));
-    accum_t<D, 4, kLookFwd>(vt, pf, o, la);
+    for (int g = 0; g < 4; ++g) {
+      pf[g] = frag_acc(sc[g >> 1], 8 * (g & 1));
+      pl[g] = frag_acc_lo(sc[g >> 1], 8 * (g & 1), pf[g]);
+    }
+    accum_t2<D, 4, kLookFwd>(vt, pf, pl, o, la);
   };
 
   run_ring2(
@@ -447,52 +536,6 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(AttnParams p) {
   }
 }
 
-// ------------------------------------------------------------------ pipelined products
-// Two accumulator chains over the D columns of LDS tiles, with the B operands
-// in registers:  s0 += A0[r0 + (0..31)] x0^T,  s1 += A1[r1 + (0..31)] x1^T.
-// The schedule keeps LA fragment reads in flight ahead of the products
-// (without it the compiler reads each fragment right before its product and
-// the LDS latency is exposed on every step).
-template <int D, int LA>
-__device__ __forceinline__ void scores2(const uint8_t* a0, int r0, const bf16x8 (&x0)[D / 16], f32x16& s0,
-                                        const uint8_t* a1, int r1, const bf16x8 (&x1)[D / 16], f32x16& s1,
-                                        LaneAddr la) {
-  constexpr int N = D / 8;               // products (and fragment reads)
-  constexpr int L = LA < N ? LA : N - 1;
-#pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
-    s0 = mfma(frag_rows<D>(a0, r0, kk, la), x0[kk], s0);
-    s1 = mfma(frag_rows<D>(a1, r1, kk, la), x1[kk], s1);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x100, L, 0);      // LDS reads
-#pragma unroll
-  for (int i = 0; i < N - L; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x008, L, 0);
-}
-
-// acc[dt] += A^T x over NG groups of 16 rows: A the LDS tile read transposed
-// (d rows, row-index contraction), x[g] a bf16 operand from registers (P^T,
-// dS^T); two reads per fragment, LA fragments in flight.
-template <int D, int NG, int LA>
-__device__ __forceinline__ void accum_t(const uint8_t* lds, const bf16x8 (&x)[NG], f32x16 (&acc)[D / 32], LaneAddr la) {
-  constexpr int N = NG * D / 32;
-  constexpr int L = LA < N ? LA : N - 1;
-#pragma unroll
-  for (int g = 0; g < NG; ++g)
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) acc[dt] = mfma(frag_cols<D>(lds, dt, g, la), x[g], acc[dt]);
-  __builtin_amdgcn_sched_group_barrier(0x100, 2 * L, 0);
-#pragma unroll
-  for (int i = 0; i < N - L; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x008, L, 0);
-}
-
 // ------------------------------------------------------------------ backward: dK, dV
 // Flat grid over (key block of 128 over all segments, kv head, split, b), key
 // block slowest: the earliest key blocks see the most query tiles, so they are
@@ -505,13 +548,13 @@ __device__ __forceinline__ void accum_t(const uint8_t* lds, const bf16x8 (&x)[NG
 // The block's 128 keys form four groups of 32, and each group has two waves
 // with different jobs, on the same SIMD (wave w runs on SIMD w % 4):
 //  * role 0 (waves 0-3) holds K, computes S^T = K Q^T, P^T = exp(S^T - lse),
-//    hands P^T (bf16) to its partner through LDS and accumulates dV^T += dO^T P^T;
+//    hands P^T (fp32) to its partner through LDS and accumulates dV^T += dO^T P^T;
 //  * role 1 (waves 4-7) holds V, computes dP^T = V dO^T, takes P^T and forms
 //    dS^T = P^T (dP^T - delta), and accumulates dK^T += Q^T dS^T.
 // Each wave then needs one operand block and one accumulator block, which fits
 // 256 registers, and the two waves of a SIMD issue different instruction mixes
-// (softmax on one, products on the other) that interleave.  Both use the same
-// bf16 P^T, the one dV is built from.
+// (softmax on one, products on the other) that interleave.  dS^T is formed
+// from the fp32 P^T and rounded to bf16 once, as in the dQ kernel.
 template <int D>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) attn_bwd_dkdv_kernel(AttnParams p) {
   constexpr int TB = QT * D * 2;
@@ -519,7 +562,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   // ds_read immediate), then the statistics and the P^T handover.
   __shared__ __attribute__((aligned(16))) uint8_t qg0[2][TB], qg1[2][TB];   // per stage: Q tile, then dO tile
   __shared__ __attribute__((aligned(16))) float st0[2][QT], st1[2][QT];             // lse, delta
-  __shared__ __attribute__((aligned(16))) u32x4 xp[4][QT / 16][64];    // P^T handover: [group][16 queries][lane]
+  // P^T handover in fp32, so that dS^T = P^T (dP^T - delta) rounds once: [group][16 queries][half][lane]
+  __shared__ __attribute__((aligned(16))) float4 xp[4][QT / 16][2][64];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave & 3, role = wave >> 2;
@@ -597,6 +641,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     // S^T from Q, dV^T from dO; role 1: dP^T from dO, dK^T from Q), so the
     // accumulators never meet at a branch join.
     f32x16 s[2] = {f32x16{}, f32x16{}};              // role 0: S^T -> P^T, role 1: dP^T -> dS^T
+    bf16x8 x[4];                                       // role 0: P^T, role 1: dS^T (bf16)
     scores2<D, kLookDkv>(qt_l, 0, kv, s[0], qt_l, 32, kv, s[1], la1);
     {
       if (role == 0) {
@@ -633,28 +678,27 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
           }
         }
 #pragma unroll
-        for (int g = 0; g < 4; ++g) xp[grp][g][lane] = __builtin_bit_cast(u32x4, frag_acc(s[g >> 1], 8 * (g & 1)));
+        for (int g = 0; g < 4; ++g) {
+          const int h = g >> 1, i0 = 8 * (g & 1);
+          x[g] = frag_acc(s[h], i0);                   // bf16 P^T for this wave's dV product
+          xp[grp][g][0][lane] = make_float4(s[h][i0], s[h][i0 + 1], s[h][i0 + 2], s[h][i0 + 3]);
+          xp[grp][g][1][lane] = make_float4(s[h][i0 + 4], s[h][i0 + 5], s[h][i0 + 6], s[h][i0 + 7]);
+        }
       }
     }
     ring_barrier();                                    // P^T of every group is visible to its partner
-    bf16x8 x[4];                                       // role 0: P^T, role 1: dS^T (bf16)
-    if (role == 0) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) x[g] = __builtin_bit_cast(bf16x8, xp[grp][g][lane]);
-    } else {
+    if (role == 1) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const u32x4 pp = xp[grp][g][lane];
+        const float4 p0 = xp[grp][g][0][lane], p1 = xp[grp][g][1][lane];
+        const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
         const int h = g >> 1, i0 = 8 * (g & 1);
         const float4 d0 = *reinterpret_cast<const float4*>(&st[1][32 * h + (i0 >> 2) * 8 + rbase]);
         const float4 d1 = *reinterpret_cast<const float4*>(&st[1][32 * h + ((i0 >> 2) + 1) * 8 + rbase]);
         const float dev[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
         float ds[8];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          ds[2 * j] = lo16(pp[j]) * (s[h][i0 + 2 * j] - dev[2 * j]);
-          ds[2 * j + 1] = hi16(pp[j]) * (s[h][i0 + 2 * j + 1] - dev[2 * j + 1]);
-        }
+        for (int j = 0; j < 8; ++j) ds[j] = pv[j] * (s[h][i0 + j] - dev[j]);
         x[g] = __builtin_bit_cast(
             bf16x8, u32x4{pack2(ds[0], ds[1]), pack2(ds[2], ds[3]), pack2(ds[4], ds[5]), pack2(ds[6], ds[7])});
       }

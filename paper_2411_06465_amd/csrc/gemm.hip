@@ -342,7 +342,13 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, int64_t m, int tn,
 #pragma unroll
               for (int j = 0; j < 8; ++j) src[j] += r[j];
             }
-            *reinterpret_cast<u32x4*>(e.own_out + off) = pack8(src);
+            if (e.own_out_f32) {
+              float4* o32 = reinterpret_cast<float4*>(e.own_out_f32 + off);
+              o32[0] = make_float4(src[0], src[1], src[2], src[3]);
+              o32[1] = make_float4(src[4], src[5], src[6], src[7]);
+            } else {
+              *reinterpret_cast<u32x4*>(e.own_out + off) = pack8(src);
+            }
           } else {
             *reinterpret_cast<u32x4*>(e.send + off) = pack8(src);
           }

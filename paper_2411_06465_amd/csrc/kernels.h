@@ -64,7 +64,7 @@ enum class EpiKind {
   StoreF32,     // C (f32) = acc, row-major with ldc
   AccF32,       // C (f32) += acc
   QkvRope,      // split [Q|K|V] columns, RoPE on Q and K, bf16
-  ResidualSP,   // own rows: bf16(acc + resid + receipt); peer rows: bf16(acc) -> send buffer
+  ResidualSP,   // own rows: bf16 or fp32 (acc + resid + receipt); peer rows: bf16(acc) -> send buffer
   SwiGLUFwd,    // gate/up tile pairs -> G, U, act, prod (bf16)
   SwiGLUBwd     // acc = d(prod) -> dG, dU from the stashed G, U, act
 };
@@ -80,6 +80,7 @@ struct EpiParams {
   int32_t d_h;
   // ResidualSP (rows in the gathered view; own rows mapped like RowSrc)
   uint16_t* own_out;    // [b*s_sp][ldc]
+  float* own_out_f32;   // when set, the own rows are stored here in fp32 instead
   const uint16_t* resid;    // may be null
   const uint16_t* receipt;  // may be null
   uint16_t* send;       // [b*(t-1)*s_sp][ldc]
@@ -122,10 +123,20 @@ hipError_t gemm_split_store(uint16_t* c, int64_t ldc, const float* partial, int6
 // also copied to x_copy when that is not null.
 hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* gain, uint16_t* y, int64_t rows,
                        int32_t h, float eps, hipStream_t stream, uint16_t* x_copy = nullptr);
-// dx = bf16(dres + d rmsnorm/dx . dy);  partial[blk][h] = sum over the block's rows of dy*xhat.
-hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const uint16_t* dy,
-                       const uint16_t* dres, uint16_t* dx, float* partial, int32_t n_partial,
-                       int64_t rows, int32_t h, float eps, hipStream_t stream);
+// RMSNorm backward: dx = dres + d rmsnorm/dx . dy, stored bf16 (and fp32 when
+// dx_f32 is set);  partial[blk][h] = sum over the block's rows of dy*xhat.
+// dy is bf16 (dy) or fp32 (dy_f32); dres is absent, bf16 or fp32.  Forms:
+// (bf16 dy, no dres), (fp32 dy, bf16 dres, fp32 copy), (fp32 dy, fp32 dres).
+struct NormBwdIo {
+  const uint16_t* dy;
+  const float* dy_f32;
+  const uint16_t* dres;
+  const float* dres_f32;
+  uint16_t* dx;
+  float* dx_f32;
+};
+hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const NormBwdIo& io, float* partial,
+                       int32_t n_partial, int64_t rows, int32_t h, float eps, hipStream_t stream);
 // out[j] += sum_i partial[i][j] in a fixed order; with more than 256 rows partial
 // is overwritten (used as scratch).
 hipError_t reduce_rows_add(float* partial, int32_t n_partial, int32_t h, float* out, hipStream_t stream);

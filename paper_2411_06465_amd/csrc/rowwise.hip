@@ -92,16 +92,48 @@ __global__ void __launch_bounds__(256) rmsnorm_fwd_kernel(const uint16_t* __rest
   }
 }
 
+// Eight consecutive values of a bf16 row (one 16-byte load) or an fp32 row (two).
+template <bool F32>
+struct Vec8 {
+  u32x4 v;
+};
+template <>
+struct Vec8<true> {
+  float4 a, b;
+};
+template <bool F32>
+__device__ __forceinline__ Vec8<F32> load8(const void* row, int c) {
+  if constexpr (F32) {
+    const float4* p = reinterpret_cast<const float4*>(row) + 2 * c;
+    return Vec8<true>{p[0], p[1]};
+  } else {
+    return Vec8<false>{reinterpret_cast<const u32x4*>(row)[c]};
+  }
+}
+template <bool F32>
+__device__ __forceinline__ void unpack(const Vec8<F32>& u, float* v) {
+  if constexpr (F32) {
+    v[0] = u.a.x; v[1] = u.a.y; v[2] = u.a.z; v[3] = u.a.w;
+    v[4] = u.b.x; v[5] = u.b.y; v[6] = u.b.z; v[7] = u.b.w;
+  } else {
+    unpack8(u.v, v);
+  }
+}
+
 // Grid-stride over rows, one 256-thread block per row: thread t owns the
-// 16-byte chunks t + 256 it (it < CPT, h <= 2048 * CPT) of every row, so it
+// 8-column chunks t + 256 it (it < CPT, h <= 2048 * CPT) of every row, so it
 // keeps its columns' partial sums of dy*xhat in registers and writes them to
 // partial[blockIdx.x][h] at the end.  The two row sums go through LDS,
 // double-buffered by row parity so one barrier per row suffices.
-template <int CPT>
+// DY32: the incoming gradient d(out) is fp32 (else bf16); RES: the residual
+// gradient added to the result is absent (0), bf16 (1) or fp32 (2); OUT32:
+// the result is also stored in fp32.
+template <int CPT, bool DY32, int RES, bool OUT32>
 __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
-    const uint16_t* __restrict__ x, const uint16_t* __restrict__ gain, const uint16_t* __restrict__ dy,
-    const uint16_t* __restrict__ dres, uint16_t* __restrict__ dx, float* __restrict__ partial,
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ gain, const void* __restrict__ dy,
+    const void* __restrict__ dres, uint16_t* __restrict__ dx, float* __restrict__ dx32, float* __restrict__ partial,
     int64_t rows, int32_t h, float eps) {
+  constexpr bool R32 = RES == 2;
   __shared__ float sums[2][4][2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nch = h / 8;
@@ -111,20 +143,23 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[it][j] = 0.f;
   const u32x4* gr = reinterpret_cast<const u32x4*>(gain);
-  u32x4 gv[CPT], xv[CPT], dv[CPT], rv[CPT], xn[CPT], dn[CPT], rn[CPT];
-  const u32x4 zero = {0u, 0u, 0u, 0u};
-  // row `row`'s x, dy and residual gradient into (a, b, r)
-  auto load_row = [&](int64_t row, u32x4 (&a)[CPT], u32x4 (&b)[CPT], u32x4 (&r)[CPT]) __attribute__((always_inline)) {
+  u32x4 gv[CPT], xv[CPT], xn[CPT];
+  Vec8<DY32> dv[CPT], dn[CPT];
+  Vec8<R32> rv[CPT], rn[CPT];
+  const int64_t dsz = DY32 ? 4 : 2, rsz = R32 ? 4 : 2;
+  // row `row`'s x, d(out) and residual gradient into (a, b, r)
+  auto load_row = [&](int64_t row, u32x4 (&a)[CPT], Vec8<DY32> (&b)[CPT], Vec8<R32> (&r)[CPT])
+                      __attribute__((always_inline)) {
     const u32x4* xr = reinterpret_cast<const u32x4*>(x + row * h);
-    const u32x4* dr = reinterpret_cast<const u32x4*>(dy + row * h);
-    const u32x4* rr = dres ? reinterpret_cast<const u32x4*>(dres + row * h) : nullptr;
+    const void* dr = static_cast<const uint8_t*>(dy) + row * h * dsz;
+    const void* rr = RES ? static_cast<const uint8_t*>(dres) + row * h * rsz : nullptr;
 #pragma unroll
     for (int it = 0; it < CPT; ++it) {
       const int c = tid + 256 * it;
       if (c < nch) {
         a[it] = xr[c];
-        b[it] = dr[c];
-        r[it] = rr ? rr[c] : zero;
+        b[it] = load8<DY32>(dr, c);
+        if constexpr (RES != 0) r[it] = load8<R32>(rr, c);
       }
     }
   };
@@ -140,7 +175,7 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
     for (int it = 0; it < CPT; ++it) {
       xv[it] = xn[it];
       dv[it] = dn[it];
-      rv[it] = rn[it];
+      if constexpr (RES != 0) rv[it] = rn[it];
     }
     // the next row's loads fly under this row's reductions and stores
     if (row + gridDim.x < rows) load_row(row + gridDim.x, xn, dn, rn);
@@ -151,7 +186,7 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
       if (c < nch) {
         float f[8], d[8], g[8];
         unpack8(xv[it], f);
-        unpack8(dv[it], d);
+        unpack<DY32>(dv[it], d);
         unpack8(gv[it], g);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -172,15 +207,21 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
     const float rstd = rsqrtf(ss / h + eps);
     const float c_mean = dot * rstd / h;        // mean over the row of (gain*dy) * xhat
     u32x4* out = reinterpret_cast<u32x4*>(dx + row * h);
+    float4* out32 = OUT32 ? reinterpret_cast<float4*>(dx32 + row * h) : nullptr;
 #pragma unroll
     for (int it = 0; it < CPT; ++it) {
       const int c = tid + 256 * it;
       if (c < nch) {
         float f[8], d[8], g[8], r[8];
         unpack8(xv[it], f);
-        unpack8(dv[it], d);
+        unpack<DY32>(dv[it], d);
         unpack8(gv[it], g);
-        unpack8(rv[it], r);      // zeros without a residual gradient
+        if constexpr (RES != 0) {
+          unpack<R32>(rv[it], r);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) r[j] = 0.f;
+        }
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const float xh = f[j] * rstd;
@@ -188,6 +229,10 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
           r[j] += rstd * (g[j] * d[j] - xh * c_mean);
         }
         out[c] = pack8(r);
+        if constexpr (OUT32) {
+          out32[2 * c] = make_float4(r[0], r[1], r[2], r[3]);
+          out32[2 * c + 1] = make_float4(r[4], r[5], r[6], r[7]);
+        }
       }
     }
   }
@@ -545,17 +590,32 @@ int32_t rmsnorm_bwd_partials(int64_t rows) {
   return static_cast<int32_t>(rows < 256 ? rows : 256);     // one block per row, one per CU
 }
 
-hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const uint16_t* dy, const uint16_t* dres,
-                       uint16_t* dx, float* partial, int32_t n_partial, int64_t rows, int32_t h, float eps,
-                       hipStream_t stream) {
+hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* gain, const NormBwdIo& io, float* partial,
+                       int32_t n_partial, int64_t rows, int32_t h, float eps, hipStream_t stream) {
   if (rows <= 0) return hipSuccess;
   const int cpl = (h + 2047) / 2048;
-#define L4D_RMS_BWD(C)                                                                                       \
-  hipLaunchKernelGGL(rmsnorm_bwd_kernel<C>, dim3(n_partial), dim3(256), 0, stream, x, gain, dy, dres, dx, \
-                     partial, rows, h, eps)
-  if (cpl <= 1) L4D_RMS_BWD(1);
-  else if (cpl <= 2) L4D_RMS_BWD(2);
-  else L4D_RMS_BWD(4);
+  const bool dy32 = io.dy_f32 != nullptr;
+  const int res = io.dres_f32 ? 2 : io.dres ? 1 : 0;
+  const bool out32 = io.dx_f32 != nullptr;
+  const void* dy = dy32 ? static_cast<const void*>(io.dy_f32) : io.dy;
+  const void* dres = res == 2 ? static_cast<const void*>(io.dres_f32) : io.dres;
+  // the three forms the layer and the LM-head block use
+#define L4D_RMS_BWD(C, D32, R, O32)                                                                            \
+  hipLaunchKernelGGL((rmsnorm_bwd_kernel<C, D32, R, O32>), dim3(n_partial), dim3(256), 0, stream, x, gain, dy, \
+                     dres, io.dx, io.dx_f32, partial, rows, h, eps)
+#define L4D_RMS_BWD_FORM(C)                                                      \
+  if (!dy32 && res == 0 && !out32) L4D_RMS_BWD(C, false, 0, false);              \
+  else if (dy32 && res == 1 && out32) L4D_RMS_BWD(C, true, 1, true);             \
+  else if (dy32 && res == 2 && !out32) L4D_RMS_BWD(C, true, 2, false);           \
+  else return hipErrorInvalidValue;
+  if (cpl <= 1) {
+    L4D_RMS_BWD_FORM(1)
+  } else if (cpl <= 2) {
+    L4D_RMS_BWD_FORM(2)
+  } else {
+    L4D_RMS_BWD_FORM(4)
+  }
+#undef L4D_RMS_BWD_FORM
 #undef L4D_RMS_BWD
   return hipGetLastError();
 }

@@ -6,7 +6,9 @@ receipt of zero, or a receipt plus zero); the table gradient is fp32 (relative
 Frobenius 5e-3), and bit-exact on every row that one token alone touches;
 LM-head: bf16 outputs (dx, the d(xn) sent to the peers) and fp32 outputs
 (loss, softmax, gain and head-weight gradients) to the bar of gpu_common,
-plus an absolute bound on the loss and the softmax.  The LM-head stash holds
+with the loss within 1e-3 absolute and dx given the flip allowance of the
+stored d(xn) it is computed from.  The whole Llama-3-8B TP4 head is compared
+in test_gpu_full_size.  The LM-head stash holds
 4 s_c b h (1 + v/h) / t bytes, the LM-head term of Sec. 3.2 divided by tc;
 the embedding stash holds the 8 b s_c bytes of int64 ids.
 """
@@ -19,7 +21,7 @@ import workloads as W
 from oracle import ends as OE
 from oracle.bf16 import from_bits
 from oracle.layer import Shard
-from gpu_common import check, dev_bf16, host_f64
+from gpu_common import bf16_ulp, check, dev_bf16, host_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -147,44 +149,16 @@ def test_lm_head_block_matches_oracle(w):
     fw, bw = head_oracle(w, inp, gs)
     assert torch.equal(got["x_kept"].view(torch.int16).cpu(), torch.from_numpy(inp["x"].view(np.int16)))
     rep, ok = [], True
-    ok &= check("xn", host_f64(got["xn"]), fw["xn"], report=rep)
-    ok &= check("loss", host_f64(got["loss"]), fw["loss"], bf16=False, report=rep)
+    ok &= check("xn", host_f64(got["xn"]), fw["xn"], contraction=False, report=rep)
+    ok &= check("loss", host_f64(got["loss"]), fw["loss"], bf16=False, abs_bound=1e-3, report=rep)
     ok &= check("probs", host_f64(got["probs"]), fw["probs"], bf16=False, report=rep)
-    ok &= check("dx", host_f64(got["dx"]), bw["dx"], report=rep)
+    x = from_bits(inp["x"])
+    rstd = 1.0 / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + w.rms_eps)
+    # dx = RMSNorm'(d(xn)) with d(xn) stored bf16: one flip of d(xn) moves dx by |g| rstd u(d(xn))
+    ok &= check("dx", host_f64(got["dx"]), bw["dx"],
+                allow=np.abs(from_bits(inp["w_norm"])) * rstd * bf16_ulp(bw["d_xn"]), report=rep)
     ok &= check("d_gain", host_f64(got["d_gain"]), bw["d_gain"], bf16=False, report=rep)
     ok &= check("d_w_lm", host_f64(got["d_w"]), bw["d_w"], bf16=False, report=rep)
     if w.tp > 1:
         ok &= check("dxn_send", host_f64(got["send"]), bw["send"], report=rep)
     assert ok, "\n".join(rep)
-    assert np.max(np.abs(host_f64(got["loss"]) - fw["loss"])) < 1e-3
-    assert np.max(np.abs(host_f64(got["probs"]) - fw["probs"])) < 1e-5
-
-
-def test_lm_head_block_full_size_sampled():
-    """The Llama-3-8B head at TP4 (8192 tokens, vocabulary shard 32064): the
-    stash against the LM-head term, and the oracle at sampled own rows (a
-    token's loss, softmax, d(xn) and dx depend on its own row only)."""
-    w = W.ENDS_LLAMA3_8B_TP4
-    print(f"\n[lm head block full size {w.name}] tokens={w.tokens} v_t={w.v_t}", flush=True)
-    inp = W.ends_inputs(w)
-    gs = 1.0 / w.tokens
-    got = run_head(w, inp, gs)
-    assert got["bytes"]["formula"] == 4 * w.s_c * w.micro_batch * (w.hidden + w.vocab) // w.tp
-    rows = np.unique(np.concatenate([[0, w.s_sp - 1], np.random.default_rng(5).choice(w.s_sp, 14, replace=False)]))
-    m = w.tp_rank * w.s_sp + rows                      # positions in the gathered token order (b = 1)
-    k = len(rows)
-    sub = Shard(hidden=w.hidden, n_heads=w.n_heads, n_kv_heads=w.n_kv_heads, ffn=w.ffn, seq=k, rms_eps=w.rms_eps)
-    x = from_bits(inp["x"])[:, rows]
-    gain, wl = from_bits(inp["w_norm"]), from_bits(inp["w_lm"])
-    tg = inp["targets"][m].reshape(1, k)
-    v0 = w.tp_rank * w.v_t
-    fw = OE.lm_head_forward(sub, x, gain, wl, tg, v0, peer_lse=inp["peer_lse"][m],
-                            peer_target_logit=inp["peer_target_logit"][m])
-    bw = OE.lm_head_backward(sub, x, gain, wl, tg, v0, fw, gs, peer_dxn=from_bits(inp["peer_dxn"])[:, rows])
-    rep, ok = [], True
-    ok &= check("loss", host_f64(got["loss"])[m], fw["loss"], bf16=False, report=rep)
-    ok &= check("probs", host_f64(got["probs"][torch.from_numpy(m).cuda()]), fw["probs"], bf16=False, report=rep)
-    ok &= check("dx", host_f64(got["dx"])[:, rows], bw["dx"], report=rep)
-    assert ok, "\n".join(rep)
-    assert np.max(np.abs(host_f64(got["loss"])[m] - fw["loss"])) < 1e-3
-    assert bool(torch.isfinite(got["d_w"]).all()) and bool(torch.isfinite(got["d_gain"]).all())

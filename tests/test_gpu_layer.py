@@ -2,8 +2,11 @@
 
 Every case runs the HIP library through its C ABI on seeded inputs and the
 CPU oracle on the same bytes, then compares every stashed tensor, every output
-and every weight gradient.  Bar: bf16 tensors max-abs <= 2e-2 and relative
-Frobenius <= 5e-3; fp32 gradient accumulators relative Frobenius <= 5e-3.
+and every weight gradient to the parity bar of gpu_common (bf16 tensors: every
+element within 2e-2 plus one bf16 step, plus the flip allowance of the stored
+operand that feeds it directly, plus for contraction outputs 6 x 5e-3 of the
+row's RMS; every tensor: relative Frobenius <= 5e-3 and per-row relative error
+<= 2e-2; the attention LSE within 2e-2 absolute).
 The stash byte count must equal Eq. 12 / (tc) exactly.
 """
 import numpy as np
@@ -12,7 +15,7 @@ import torch
 
 import workloads as W
 from oracle import memory as OM
-from gpu_common import Buffers, check, host_f64, oracle_layer
+from gpu_common import Buffers, compare_layer, oracle_layer
 
 pytestmark = pytest.mark.gpu
 
@@ -50,22 +53,7 @@ def test_layer_matches_oracle(name):
     assert saved["_bytes"]["formula"] == OM.act_bytes_per_layer(
         w.hidden, w.n_heads, w.n_kv_heads, w.ffn, w.seq, w.micro_batch, w.tp, w.cp)
 
-    rep, ok = [], True
-    for n in ("x", "xn1", "q", "k", "v", "ctx", "h1", "xn2", "gate", "up", "act", "prod"):
-        ok &= check("stash." + n, host_f64(saved[n]), fw[n], report=rep)
-    ok &= check("lse", host_f64(saved["lse"]), fw["lse"], bf16=False, report=rep)
-    ok &= check("y", host_f64(buf.y), fw["y"], report=rep)
-    ok &= check("dx", host_f64(buf.dx), bw["dx"], report=rep)
-    for n in ("norm1", "qkv", "o", "norm2", "gate_up", "down"):
-        ok &= check("d_" + n, host_f64(buf.grads[n]), bw["d_" + n], bf16=False, report=rep)
-    if w.cp > 1:
-        ok &= check("d_remote_k", host_f64(buf.d_remote[0]), bw["d_remote_k"], report=rep)
-        ok &= check("d_remote_v", host_f64(buf.d_remote[1]), bw["d_remote_v"], report=rep)
-    if w.tp > 1:
-        ok &= check("o_send", host_f64(saved["o_partial"]), fw["o_send"], report=rep)
-        ok &= check("ffn_send", host_f64(saved["ffn_partial"]), fw["ffn_send"], report=rep)
-        ok &= check("dxn2_send", host_f64(buf.sends["dxn2_partial"]), bw["dxn2_send"], report=rep)
-        ok &= check("dxn1_send", host_f64(buf.sends["dxn1_partial"]), bw["dxn1_send"], report=rep)
+    ok, rep = compare_layer(w, buf, saved, fw, bw)
     assert ok, "\n".join(rep)
 
 

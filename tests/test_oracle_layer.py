@@ -393,52 +393,3 @@ def test_lm_head_vocab_parallel_composes():
         assert np.allclose(o["loss"], ref["loss"], rtol=1e-12)
     assert np.allclose(sum(o["d_hidden"] for o in outs), ref["d_hidden"], rtol=1e-11, atol=1e-14)
     assert np.allclose(np.concatenate([o["d_w"] for o in outs]), ref["d_w"], rtol=1e-11, atol=1e-14)
-
-
-# ---------------------------------------------------------------- sampled-row forms
-
-def _sp_peers(sh):
-    p = make_peers(sh)
-    if sh.t > 1:
-        n = (sh.t - 1) * sh.s_sp
-        for name in ("sp_peer_xn1", "sp_peer_xn2", "sp_peer_dy", "sp_peer_dh1"):
-            p[name] = randn(sh.b, n, sh.h)
-        p["sp_peer_o"] = randn(sh.b, sh.s_sp, sh.h)
-        p["sp_peer_ffn"] = randn(sh.b, sh.s_sp, sh.h)
-    if sh.c > 1:
-        p["cp_peer_dk"] = randn(sh.b, sh.s_c, sh.k_t * sh.d_h, scale=0.05)
-        p["cp_peer_dv"] = randn(sh.b, sh.s_c, sh.k_t * sh.d_h, scale=0.05)
-    return {k: round_bf16(v) for k, v in p.items()}
-
-
-@pytest.mark.parametrize("t,c,r_t,r_c", [(1, 1, 0, 0), (2, 1, 1, 0), (1, 2, 0, 1), (2, 2, 1, 1)])
-def test_forward_rows_equals_full_forward_at_those_rows(t, c, r_t, r_c):
-    # The sampled-row forward used for full-size checks is the full forward
-    # restricted to the rows asked for (same rounding points).
-    sh = small_shard(seq=32, micro_batch=2, tp=t, cp=c, tp_rank=r_t, cp_rank=r_c)
-    w = {n: round_bf16(v) for n, v in make_weights(sh).items()}
-    x = round_bf16(randn(sh.b, sh.s_sp, sh.h))
-    peers = _sp_peers(sh)
-    full = Lr.layer_forward(sh, w, x, peers)
-    rows = np.array([0, 3, sh.s_sp - 1])
-    part = Lr.layer_forward_rows(sh, w, x, rows, peers)
-    m = sh.tp_rank * sh.s_sp + rows
-    close = lambda a, b: np.allclose(a, b, rtol=1e-12, atol=1e-12)
-    for name in ("y", "x", "xn1", "h1", "xn2"):
-        assert close(part[name], full[name][:, rows]), name
-    for name in ("q", "k", "v", "ctx", "gate", "up", "act", "prod"):
-        assert close(part[name], full[name][:, m]), name
-    assert close(part["lse"], full["lse"][:, :, m])
-
-
-@pytest.mark.parametrize("c,r_c", [(1, 0), (2, 0), (2, 1)])
-def test_backward_last_rows_equals_full_backward(c, r_c):
-    sh = small_shard(seq=32, micro_batch=2, cp=c, cp_rank=r_c)
-    w = {n: round_bf16(v) for n, v in make_weights(sh).items()}
-    x = round_bf16(randn(sh.b, sh.s_sp, sh.h))
-    dy = round_bf16(randn(sh.b, sh.s_sp, sh.h))
-    peers = _sp_peers(sh)
-    full = Lr.layer_backward(sh, w, Lr.layer_forward(sh, w, x, peers), dy, peers)
-    n_last = 5
-    dx = Lr.layer_backward_last_rows(sh, w, x, dy, n_last, peers)
-    assert np.allclose(dx, full["dx"][:, -n_last:], rtol=1e-12, atol=1e-12)
