@@ -3,19 +3,21 @@
 A step is one pass of the hot path on a fixed synthetic batch: the memory
 estimate (host), the layer forward (which reserves the activation stash) and
 the layer backward (which adds into fp32 weight-gradient accumulators).  The
-headline workload is the Llama-2-7B-shaped layer (h 4096, 32/32 heads,
-FFN 11008, seq 4096, micro-batch 1, TP1 CP1); the other shard shapes
-(Llama-3-8B at TP2 CP2, Llama-3-70B at TP8, the Llama-3-8B LM head at TP4)
-are reported alongside under "other_workloads", and "first_stage_1f1b" plays
-the first pipeline stage of the 70B (t, c, p) = (8, 1, 8) layout under 1F1B
-with the real kernels (10 layers x 8 micro-batches) and compares its peak live
-stash with the memory model's L layers.  "optimizer_step" times the Adam
-update of that layout's optimizer shard (the 1/(d c) of a rank's parameters
-whose fp32 master, momentum and variance it owns, d c = 4): 30 bytes of HBM
-traffic per parameter, against the HBM peak.  "model_ends" times the LM-head
-block (final RMSNorm, FP32 logits kept as the softmax, cross-entropy, forward
-and backward) and the embedding of the Llama-3-8B TP4 rank, with their stash
-bytes against the LM-head and embedding terms of the memory model.
+headline workload is the Llama-3-70B shard at TP8 inside the (TP, CP, PP, MBS)
+= (8, 1, 8, 1) layout (h 8192, 8 q / 1 kv heads per GPU, FFN shard 3584 of
+28672, seq 8192, micro-batch 1).  The Llama-3-8B shard at TP2 CP2 and the
+Llama-2-7B layer follow under "other_workloads" with the same per-kernel
+table and roofline; the Llama-3-8B LM head at TP4 is timed alongside, and
+"first_stage_1f1b" plays the first pipeline stage of the 70B (t, c, p) =
+(8, 1, 8) layout under 1F1B with the real kernels (10 layers x 8
+micro-batches) and compares its peak live stash with the memory model's L
+layers.  "optimizer_step" times the Adam update of that layout's optimizer
+shard (the 1/(d c) of a rank's parameters whose fp32 master, momentum and
+variance it owns, d c = 4): 30 bytes of HBM traffic per parameter, against the
+HBM peak.  "model_ends" times the LM-head block (final RMSNorm, FP32 logits
+kept as the softmax, cross-entropy, forward and backward) and the embedding of
+the Llama-3-8B TP4 rank, with their stash bytes against the LM-head and
+embedding terms of the memory model.
 
 Throughput is model FLOPs (forward GEMMs + causal attention over the
 unmasked query/key pairs, times 3 for forward + backward) per second.  Kernel
@@ -25,13 +27,14 @@ per-kernel table, which also names the dominant kernel), and around the
 dominant kernel's launches only in the timed steps (the roofline figure).
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline] [--no-others]
+    python bench.py --workload NAME [--steps K] [--warmup W]   # one layer workload alone
     python bench.py --calibrate-copy BYTES     # a plain device copy, for HBM counter calibration
     python bench.py --optimizer-only [--steps K] [--warmup W]   # the Adam step alone
 
 roofline.traffic is the dominant kernel's HBM bytes per launch as measured
 by rocprofv3 FETCH_SIZE + WRITE_SIZE (scaled by the counters' reading for a
-plain copy of known size), read from profiles/hbm_traffic_llama2_7b_layer.txt;
-it is null when that file has no entry for the kernel or when the kernel's
+plain copy of known size), read from profiles/hbm_traffic_<workload>.txt; it
+is null when that file has no entry for the kernel or when the kernel's
 source file has changed since the counters were taken (SHA-256 mismatch).
 """
 import argparse
@@ -102,8 +105,12 @@ def lm_flops(w):
 # Source file of each kernel family (for the traffic table's staleness check).
 KERNEL_SOURCE = {"gemm": "gemm.hip", "attn": "attention.hip", "rmsnorm": "rowwise.hip", "reduce": "rowwise.hip",
                  "rope": "rowwise.hip", "xent": "rowwise.hip", "adam": "optim.hip"}
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama2_7b_layer.txt")
 ADAM_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_adam_70b_shard.txt")
+
+
+def traffic_file(w):
+    """Counter summary of one layer workload: profiles/hbm_traffic_<name>.txt."""
+    return os.path.join(ROOT, "profiles", f"hbm_traffic_{w.name.replace('-', '_')}.txt")
 
 
 def source_sha(kernel):
@@ -114,7 +121,7 @@ def source_sha(kernel):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(kernel, path=TRAFFIC_FILE):
+def measured_traffic(kernel, path):
     """HBM bytes per launch from the committed counter summary, or None when
     absent or taken on a different version of the kernel's source."""
     if not os.path.exists(path):
@@ -181,7 +188,7 @@ def run_layer(w, steps, warmup, profile):
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    kernels, timed = {}, {}
+    kernels, timed, sequence = {}, {}, []
     if profile:
         # Untimed profiled steps: an event pair around every launch gives the
         # per-kernel table and picks the kernel with the largest share.
@@ -193,6 +200,9 @@ def run_layer(w, steps, warmup, profile):
         torch.cuda.synchronize()
         L.l4d_profile_enable(False)
         kernels = L.l4d_profile_dump()
+        order = L.l4d_profile_order()
+        per_step = len(order) // profile
+        sequence = order[:per_step]
         work = kernel_work(w)
         dom = max((k for k in kernels if k in work), key=lambda k: kernels[k][1])
         # The timed steps carry events only around that kernel (every launch's
@@ -211,7 +221,55 @@ def run_layer(w, steps, warmup, profile):
         L.l4d_profile_only(None)
     stash = est["act_bytes_per_layer"]
     arena.destroy()
-    return (t1 - t0) / steps, kernels, timed, stash
+    return (t1 - t0) / steps, kernels, timed, stash, sequence
+
+
+def layer_entry(w, steps, warmup):
+    """One layer workload: throughput over `steps` timed steps, the per-kernel
+    table, the roofline of the kernel with the largest share and the launch
+    sequence of one step."""
+    prof_steps = max(3, steps // 4)
+    sec, kernels, timed, stash, sequence = run_layer(w, steps, warmup, profile=prof_steps)
+    flops, _, _ = layer_flops(w)
+    value = flops / sec / 1e12
+    work = kernel_work(w)
+    dom = next(iter(timed))
+    launches, total_ms = timed[dom]
+    avg_s = total_ms / launches / 1e3
+    kind, amount = work[dom]
+    if kind == "mfma":
+        roof = {"bound": "mfma", "achieved": round(amount / avg_s / 1e12, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(amount / avg_s / 1e9, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = measured_traffic(dom, traffic_file(w))
+    roof["kernel"] = dom
+    roof["avg_ms"] = round(total_ms / launches, 4)
+    kern = {}
+    for k, (n, ms) in sorted(kernels.items(), key=lambda kv: -kv[1][1]):
+        e = {"launches_per_step": n / prof_steps, "ms_per_step": round(ms / prof_steps, 4)}
+        if k in work:
+            kind_k, amt = work[k]
+            per_launch_s = ms / n / 1e3
+            if kind_k == "mfma":
+                e["tflops"] = round(amt / per_launch_s / 1e12, 1)
+            else:
+                e["gbs"] = round(amt / per_launch_s / 1e9, 1)
+        kern[k] = e
+    return {"workload": describe(w), "tflops": round(value, 2), "ms_per_step": round(sec * 1e3, 4),
+            "pct_of_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2), "model_flops_per_step": flops,
+            "stash_bytes_per_layer": stash, "roofline": roof, "kernels": kern,
+            "kernels_note": f"per-kernel table from {prof_steps} untimed steps with events around every launch; "
+                            f"the timed steps carry events around {dom} only",
+            "launch_sequence": sequence}
+
+
+def describe(w):
+    return (f"{w.name}: decoder-layer shard, forward+backward, hidden {w.hidden}, {w.a_t} q / {w.k_t} kv heads per "
+            f"GPU (d_h {w.d_h}), FFN shard {w.f_t} of {w.ffn}, local tokens {w.s_c} of seq {w.seq}"
+            f"{f' (+{w.seq - w.s_c} remote K/V tokens)' if w.cp > 1 else ''}, micro-batch {w.micro_batch}, "
+            f"TP{w.tp} CP{w.cp}, rank ({w.tp_rank}, {w.cp_rank})")
 
 
 def run_first_stage_1f1b(w):
@@ -411,10 +469,22 @@ def run_lm(w, steps, warmup):
     return (time.perf_counter() - t0) / steps
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, seq):
-    """The oracle (float64 numpy, as written) on the same layer: same
-    hidden/heads/FFN, sequence `seq` (the default 4096 is the whole workload,
-    about 10-20 s on a 16-thread host)."""
+    """The oracle (float64 numpy, as written) on a bounded sample of the same
+    shard: the same hidden size, heads, FFN shard and (TP, CP) layout at global
+    sequence `seq` instead of the workload's (the default keeps it to 10-30 s
+    of CPU work)."""
     from threadpoolctl import threadpool_info
     import workloads as W
     from oracle import layer as OL
@@ -433,8 +503,11 @@ def cpu_baseline(w, seq):
     flops, _, _ = layer_flops(ws)
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"{ws.name}: one layer fwd+bwd at seq {seq}{' (the whole workload)' if seq == w.seq else ''} "
-                      f"(h {w.hidden}, {w.n_heads}/{w.n_kv_heads} heads, FFN {w.ffn}), float64 numpy, {dt:.1f} s wall"}
+            "cpu_model": cpu_model(), "logical_cpus": os.cpu_count(),
+            "sample": f"{ws.name}: one shard fwd+bwd at global seq {seq}"
+                      f"{' (the whole workload)' if seq == w.seq else f' of the workload {w.seq}'} (h {w.hidden}, "
+                      f"{w.a_t}/{w.k_t} heads and FFN shard {w.f_t} per rank, TP{w.tp} CP{w.cp}), "
+                      f"{flops / 1e12:.3f} TFLOP, float64 numpy, {dt:.1f} s wall"}
 
 
 def main():
@@ -444,7 +517,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-others", action="store_true")
-    ap.add_argument("--cpu-seq", type=int, default=4096, help="sequence of the oracle's CPU run (4096: the whole layer)")
+    ap.add_argument("--cpu-seq", type=int, default=2048,
+                    help="sequence of the oracle's CPU sample of the headline shard (8192: the whole workload)")
+    ap.add_argument("--workload", default="", help="time one layer workload alone and print its object")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
     ap.add_argument("--optimizer-only", action="store_true",
                     help="time only the Adam step over the 70B optimizer shard and print its object")
@@ -468,71 +543,48 @@ def main():
               flush=True)
         return
 
-    w = W.LLAMA2_7B
-    prof_steps = max(3, args.steps // 4)
-    sec, kernels, timed, stash = run_layer(w, args.steps, args.warmup, profile=prof_steps)
-    flops, gemm_fwd, attn_fwd = layer_flops(w)
-    value = flops / sec / 1e12
+    layers = {lw.name: lw for lw in (W.LLAMA3_70B_TP8, W.LLAMA3_8B_TP2CP2, W.LLAMA2_7B)}
+    if args.workload:
+        if args.workload not in layers:
+            print(f"unknown workload {args.workload}; one of {sorted(layers)}", file=sys.stderr)
+            sys.exit(2)
+        print(json.dumps({args.workload: layer_entry(layers[args.workload], args.steps, args.warmup)}), flush=True)
+        return
 
-    # roofline of the kernel with the largest share, timed over the timed steps
-    work = kernel_work(w)
-    dom = next(iter(timed))
-    launches, total_ms = timed[dom]
-    avg_s = total_ms / launches / 1e3
-    kind, amount = work[dom]
-    if kind == "mfma":
-        roof = {"bound": "mfma", "achieved": round(amount / avg_s / 1e12, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": round(amount / avg_s / 1e9, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = measured_traffic(dom)
-    roof["kernel"] = dom
-    roof["avg_ms"] = round(total_ms / launches, 4)
-
-    kern = {}
-    for k, (n, ms) in sorted(kernels.items(), key=lambda kv: -kv[1][1]):
-        e = {"launches_per_step": n / prof_steps, "ms_per_step": round(ms / prof_steps, 4)}
-        if k in work:
-            kind_k, amt = work[k]
-            per_launch_s = ms / n / 1e3
-            if kind_k == "mfma":
-                e["tflops"] = round(amt / per_launch_s / 1e12, 1)
-            else:
-                e["gbs"] = round(amt / per_launch_s / 1e9, 1)
-        kern[k] = e
-
+    # Headline: the Llama-3-70B shard at TP8 (the largest layer shard, and a
+    # target shape); the Llama-3-8B TP2 CP2 shard and the Llama-2-7B layer
+    # follow with the same per-kernel table and roofline.
+    w = W.LLAMA3_70B_TP8
+    head = layer_entry(w, args.steps, args.warmup)
+    torch.cuda.empty_cache()
     out = {
         "metric": "TFLOP/s per GPU, Llama layer fwd+bwd shard; % of bf16 MFMA peak",
-        "value": round(value, 2),
+        "value": head["tflops"],
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(sec * 1e3, 4),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "llama2-7b-shaped decoder layer, forward+backward shard: hidden 4096, 32 q / 32 kv "
-                               "heads (d_h 128), FFN 11008, seq 4096, micro-batch 1, TP1 CP1",
-                   "global_batch": 1, "seq_len": w.seq, "parallelism": "tp1-cp1 (one rank)",
-                   "model_flops_per_step": flops, "stash_bytes_per_layer": stash},
-        "pct_of_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
-        "roofline": roof,
-        "kernels": kern,
-        "kernels_note": f"per-kernel table from {prof_steps} untimed steps with events around every launch; "
-                        f"the timed steps carry events around {dom} only",
+        "config": {"workload": head["workload"], "global_batch": w.micro_batch, "seq_len": w.seq,
+                   "parallelism": f"tp{w.tp}-cp{w.cp}-pp{w.pp} shard (one rank of {w.n_gpus})",
+                   "model_flops_per_step": head["model_flops_per_step"],
+                   "stash_bytes_per_layer": head["stash_bytes_per_layer"]},
+        "pct_of_bf16_peak": head["pct_of_bf16_peak"],
+        "roofline": head["roofline"],
+        "kernels": head["kernels"],
+        "kernels_note": head["kernels_note"],
+        "launch_sequence": head["launch_sequence"],
     }
 
     if not args.no_others:
         others = {}
-        for ow in (W.LLAMA3_8B_TP2CP2, W.LLAMA3_70B_TP8):
-            s2, _, _, _ = run_layer(ow, max(5, args.steps // 2), 2, profile=0)
-            f2, _, _ = layer_flops(ow)
-            others[ow.name] = {"tflops": round(f2 / s2 / 1e12, 2), "ms_per_step": round(s2 * 1e3, 3),
-                               "pct_of_bf16_peak": round(100 * f2 / s2 / 1e12 / PEAK_BF16_TFLOPS, 2)}
+        for ow in (W.LLAMA3_8B_TP2CP2, W.LLAMA2_7B):
+            others[ow.name] = layer_entry(ow, args.steps, args.warmup)
             torch.cuda.empty_cache()
         lw = W.LLAMA3_8B_LM_TP4
         s3 = run_lm(lw, max(5, args.steps // 2), 2)
