@@ -262,6 +262,24 @@ int lm_head_xent(int64_t n_tokens, int64_t hidden, int64_t vocab_shard, int64_t 
                  const float* peer_lse, const float* peer_target_logit, float grad_scale,
                  float* loss, void* d_hidden, float* d_w_lm, l4d_arena* arena, void* hip_stream);
 
+/* lm_head_xent without an arena, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, layouts, results and errors as
+ * lm_head_xent, minus the arena: the logits (and, for a vocabulary shard with
+ * a ragged tail, the fp32 sum of d_hidden) live in a 64 MiB array of device
+ * memory that the library holds per GPU, i.e. n_tokens * vocab_shard * 2
+ * bytes, rounded up to 256, plus n_tokens * hidden * 4 for a ragged shard,
+ * must fit in 67,108,864 bytes (e.g. 1024 tokens of a 32000-wide shard);
+ * larger problems return L4D_EINVAL before anything is launched.  The call
+ * itself allocates nothing (the first call on a device looks up that
+ * device's array once).  Every call on one GPU uses the same array: calls
+ * that overlap on one device (concurrent streams, or threads) race and give
+ * wrong results; calls ordered on one stream are safe. */
+int lm_head_xent_noalloc(int64_t n_tokens, int64_t hidden, int64_t vocab_shard, int64_t vocab_start,
+                         const void* hidden_states, const void* w_lm, const int64_t* targets,
+                         const float* peer_lse, const float* peer_target_logit, float grad_scale,
+                         float* loss, void* d_hidden, float* d_w_lm, void* hip_stream);
+
 /* ------------------------------------------------------------------------
  * The ends of the model (Sec. 3.2: the embedding and LM-head activation terms)
  *

@@ -96,6 +96,7 @@ def lib():
                                  C.POINTER(PeerInputs), C.POINTER(PeerOutputs), P, P, P, C.POINTER(LayerGrads),
                                  P, P, P, P], C.c_int),
             "lm_head_xent": ([i64, i64, i64, i64, P, P, P, P, P, f32, P, P, P, P, P], C.c_int),
+            "lm_head_xent_noalloc": ([i64, i64, i64, i64, P, P, P, P, P, f32, P, P, P, P], C.c_int),
             "l4d_adam_step": ([C.POINTER(Adam), i64, P, P, P, P, P, P], C.c_int),
             "embedding_fwd": ([C.POINTER(Model), C.POINTER(Parallel), P, P, P, P, P, P, C.POINTER(P), P], C.c_int),
             "embedding_bwd": ([C.POINTER(Model), C.POINTER(Parallel), P, P, P, P, P, P], C.c_int),
@@ -271,6 +272,16 @@ def lm_head_xent(hidden, w_lm, targets, loss, d_hidden, d_w_lm, arena, vocab_sta
     _check(lib().lm_head_xent(n, h, v_t, vocab_start, _ptr(hidden), _ptr(w_lm), _ptr(targets), _ptr(peer_lse),
                               _ptr(peer_target_logit), grad_scale, _ptr(loss), _ptr(d_hidden), _ptr(d_w_lm),
                               arena.h, _stream(stream)))
+
+
+def lm_head_xent_noalloc(hidden, w_lm, targets, loss, d_hidden, d_w_lm, vocab_start=0, peer_lse=None,
+                         peer_target_logit=None, grad_scale=1.0, stream=None):
+    """lm_head_xent with the library's per-GPU static workspace instead of an arena."""
+    n, h = hidden.shape
+    v_t = w_lm.shape[0]
+    _check(lib().lm_head_xent_noalloc(n, h, v_t, vocab_start, _ptr(hidden), _ptr(w_lm), _ptr(targets),
+                                      _ptr(peer_lse), _ptr(peer_target_logit), grad_scale, _ptr(loss),
+                                      _ptr(d_hidden), _ptr(d_w_lm), _stream(stream)))
 
 
 # ------------------------------------------------------------------ the ends of the model

@@ -986,25 +986,37 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
 
 // ============================================================== LM head
 
-extern "C" int lm_head_xent(int64_t n, int64_t h, int64_t v_t, int64_t v0, const void* hidden, const void* w_lm,
-                            const int64_t* targets, const float* peer_lse, const float* peer_z, float grad_scale,
-                            float* loss, void* d_hidden, float* d_w, l4d_arena* A, void* stream_ptr) {
+namespace {
+// Bytes of workspace the LM head needs: the bf16 logits, plus an fp32 n x h
+// sum of d_hidden when the vocabulary shard has a ragged tail (ragged_k_split).
+uint64_t lm_xent_ws_bytes(int64_t n, int64_t h, int64_t v_t) {
+  return align_up((uint64_t)n * v_t * 2) + (ragged_k_split(v_t) ? align_up((uint64_t)n * h * 4) : 0);
+}
+
+int lm_xent_check(int64_t n, int64_t h, int64_t v_t, int64_t v0, const void* hidden, const void* w_lm,
+                  const int64_t* targets, const float* peer_lse, const float* peer_z, const float* loss,
+                  const void* d_hidden, const float* d_w) {
   if (n < 0 || h <= 0 || v_t <= 0 || v0 < 0) return fail(L4D_EINVAL, "bad LM-head sizes");
   if (h % 8 || v_t % 8) return fail(L4D_EINVAL, "hidden and vocab shard must be multiples of 8");
   if (n * v_t > ((int64_t)1 << 40) || n > INT32_MAX || v_t > INT32_MAX) return fail(L4D_EINVAL, "problem too large");
-  if (!hidden || !w_lm || !targets || !loss || !d_hidden || !d_w || !A)
-    return fail(L4D_EINVAL, "hidden, w_lm, targets, loss, d_hidden, d_w_lm and arena are required");
+  if (!hidden || !w_lm || !targets || !loss || !d_hidden || !d_w)
+    return fail(L4D_EINVAL, "hidden, w_lm, targets, loss, d_hidden and d_w_lm are required");
   if ((peer_lse == nullptr) != (peer_z == nullptr))
     return fail(L4D_EINVAL, "peer_lse and peer_target_logit go together");
-  if (n == 0) return L4D_OK;
-  hipStream_t s = static_cast<hipStream_t>(stream_ptr);
-  Workspace ws;
+  return L4D_OK;
+}
+
+// The LM-head kernel sequence over lm_xent_ws_bytes(n, h, v_t) bytes of
+// device workspace at ws (256-byte aligned; nothing in it needs to start at
+// zero: every byte is written before it is read).
+int lm_xent_run(int64_t n, int64_t h, int64_t v_t, int64_t v0, const void* hidden, const void* w_lm,
+                const int64_t* targets, const float* peer_lse, const float* peer_z, float grad_scale, float* loss,
+                void* d_hidden, float* d_w, uint8_t* ws, hipStream_t s) {
   const uint64_t logit_bytes = align_up((uint64_t)n * v_t * 2);
   const bool split_k = ragged_k_split(v_t);
-  int rc = take_ws(A, logit_bytes + (split_k ? (uint64_t)n * h * 4 : 0), ws);
-  if (rc) return rc;
-  uint16_t* logits = reinterpret_cast<uint16_t*>(A->base + ws.off);
-  float* dh_f32 = split_k ? reinterpret_cast<float*>(A->base + ws.off + logit_bytes) : nullptr;
+  uint16_t* logits = reinterpret_cast<uint16_t*>(ws);
+  float* dh_f32 = split_k ? reinterpret_cast<float*>(ws + logit_bytes) : nullptr;
+  int rc;
   if ((rc = run_gemm("gemm_lm_logits", s, n, v_t, h, op(RowSrc::plain(hidden, h), n), Layout::KC,
                      op(RowSrc::plain(w_lm, h), v_t), Layout::KC, epi_store(logits, v_t))))
     return rc;
@@ -1037,6 +1049,63 @@ extern "C" int lm_head_xent(int64_t n, int64_t h, int64_t v_t, int64_t v0, const
   }
   return run_gemm("gemm_lm_dw", s, v_t, h, n, op(RowSrc::plain(logits, v_t), v_t), Layout::MN,
                   op(RowSrc::plain(hidden, h), h), Layout::MN, epi_acc(d_w, h));
+}
+
+// Workspace of lm_head_xent_noalloc: one array per device, held by the loaded
+// code object until the process ends.  Host code must use the address that
+// hipGetSymbolAddress returns for the current device, never the array's name.
+constexpr uint64_t kScratchBytes = 64ull << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address, resolved once per device.
+int scratch_on_current_device(uint8_t** out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(L4D_EDEVICE, "device %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(L4D_EDEVICE, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = static_cast<uint8_t*>(g_scratch_ptr[dev]);
+  return L4D_OK;
+}
+}  // namespace
+
+extern "C" int lm_head_xent(int64_t n, int64_t h, int64_t v_t, int64_t v0, const void* hidden, const void* w_lm,
+                            const int64_t* targets, const float* peer_lse, const float* peer_z, float grad_scale,
+                            float* loss, void* d_hidden, float* d_w, l4d_arena* A, void* stream_ptr) {
+  int rc = lm_xent_check(n, h, v_t, v0, hidden, w_lm, targets, peer_lse, peer_z, loss, d_hidden, d_w);
+  if (rc) return rc;
+  if (!A) return fail(L4D_EINVAL, "arena is required");
+  if (n == 0) return L4D_OK;
+  Workspace ws;
+  if ((rc = take_ws(A, lm_xent_ws_bytes(n, h, v_t), ws))) return rc;
+  return lm_xent_run(n, h, v_t, v0, hidden, w_lm, targets, peer_lse, peer_z, grad_scale, loss, d_hidden, d_w,
+                     reinterpret_cast<uint8_t*>(A->base + ws.off), static_cast<hipStream_t>(stream_ptr));
+}
+
+extern "C" int lm_head_xent_noalloc(int64_t n, int64_t h, int64_t v_t, int64_t v0, const void* hidden,
+                                    const void* w_lm, const int64_t* targets, const float* peer_lse,
+                                    const float* peer_z, float grad_scale, float* loss, void* d_hidden, float* d_w,
+                                    void* stream_ptr) {
+  int rc = lm_xent_check(n, h, v_t, v0, hidden, w_lm, targets, peer_lse, peer_z, loss, d_hidden, d_w);
+  if (rc) return rc;
+  const uint64_t need = lm_xent_ws_bytes(n, h, v_t);
+  if (need > kScratchBytes)
+    return fail(L4D_EINVAL, "LM head needs %llu bytes of workspace; the static scratch holds %llu",
+                (unsigned long long)need, (unsigned long long)kScratchBytes);
+  if (n == 0) return L4D_OK;
+  uint8_t* ws = nullptr;
+  if ((rc = scratch_on_current_device(&ws))) return rc;
+  return lm_xent_run(n, h, v_t, v0, hidden, w_lm, targets, peer_lse, peer_z, grad_scale, loss, d_hidden, d_w, ws,
+                     static_cast<hipStream_t>(stream_ptr));
 }
 
 // ============================================================== the ends of the model

@@ -263,3 +263,12 @@ def test_mem_fit_equals_the_oracle_on_every_printed_run():
         assert L.mem_fit(dict(base, total_bytes=total), 40 * gib) == fit
     with pytest.raises(L.L4DError):
         L.mem_fit(base, 0)
+
+
+def test_lm_head_noalloc_rejects_oversized_problems_before_touching_the_device():
+    # 2048 tokens x a 32064-wide shard need 131 MB of logits: more than the 64 MiB static workspace
+    lib = L.lib()
+    f = C.c_void_p(FAKE_BASE)
+    rc = lib.lm_head_xent_noalloc(2048, 4096, 32064, 0, f, f, f, f, f, 1.0, f, f, f, None)
+    assert rc == L.L4D_EINVAL
+    assert "static scratch" in lib.l4d_last_error().decode()
