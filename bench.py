@@ -517,7 +517,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-others", action="store_true")
-    ap.add_argument("--cpu-seq", type=int, default=2048,
+    ap.add_argument("--cpu-seq", type=int, default=8192,
                     help="sequence of the oracle's CPU sample of the headline shard (8192: the whole workload)")
     ap.add_argument("--workload", default="", help="time one layer workload alone and print its object")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
