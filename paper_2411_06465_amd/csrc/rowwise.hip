@@ -324,11 +324,13 @@ __global__ void rope_table_kernel(float2* tab, ChunkMap map, int32_t rows, int32
 
 // ------------------------------------------------------------------ cross-entropy
 // One 256-thread block per token row of bf16 logits [n][v_t] (v_t % 8 == 0).
+// logits and dlogits may be the same buffer (the LM head overwrites the logits
+// with their gradient in place), so neither is declared __restrict__.
 
 __global__ void __launch_bounds__(256) xent_rows_kernel(
-    const uint16_t* __restrict__ logits, int32_t v_t, int64_t v0, const int64_t* __restrict__ targets,
+    const uint16_t* logits, int32_t v_t, int64_t v0, const int64_t* __restrict__ targets,
     const float* __restrict__ peer_lse, const float* __restrict__ peer_z, float grad_scale,
-    float* __restrict__ loss, uint16_t* __restrict__ dlogits) {
+    float* __restrict__ loss, uint16_t* dlogits) {
   __shared__ float red_m[4], red_s[4];
   __shared__ float bcast;
   const int64_t row = blockIdx.x;

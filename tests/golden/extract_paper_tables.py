@@ -1,16 +1,15 @@
 """Recipe that wrote ``paper_memory_tables.json`` and ``paper_oom_outcomes.json``.
 
-It reads the LaTeX source of arXiv 2411.06465 (mounted read-only at
-/root/reference/PAPER.md in the build container; not present elsewhere) and
-copies, cell by cell, the values the paper prints in its memory-estimate tables
-(Tables "a100-memory-table", "a100-memory-table-70b",
+It reads the LaTeX source of arXiv 2411.06465 (its path is the one required
+argument) and copies, cell by cell, the values the paper prints in its
+memory-estimate tables (Tables "a100-memory-table", "a100-memory-table-70b",
 "h100-memory-table-8B-8192", "h100-memory-table-8B-16384",
 "h100-memory-table-8B-32768") and the OOM / TFLOP/s outcomes of its
 throughput tables.  Nothing here computes anything: the outputs are the
 paper's printed numbers plus the table label, caption facts (model, sequence
 length, GPU memory) and the colour of each cell.
 
-Run:  python tests/golden/extract_paper_tables.py /root/reference/PAPER.md
+Run:  python tests/golden/extract_paper_tables.py <LaTeX source of the paper>
 """
 import json
 import re
@@ -84,4 +83,6 @@ def main(path):
 
 
 if __name__ == "__main__":
-    main(sys.argv[1] if len(sys.argv) > 1 else "/root/reference/PAPER.md")
+    if len(sys.argv) != 2:
+        sys.exit("usage: extract_paper_tables.py <LaTeX source of the paper>")
+    main(sys.argv[1])

@@ -6,6 +6,7 @@ import torch
 
 import paper_2411_06465_amd as L
 import workloads as W
+from oracle import memory as OM
 from paper_2411_06465_amd.pipeline import run_first_stage
 
 pytestmark = pytest.mark.gpu
@@ -30,10 +31,12 @@ def test_first_stage_peak_is_L_layers(pp, m):
     arena = L.Arena.on(torch.empty(w.n_layers * per + max(fws, bws) + (1 << 20), dtype=torch.uint8, device="cuda"))
     r = run_first_stage(model, par, weights, w.n_layers // pp, m, x, dy, grads, arena)
     torch.cuda.synchronize()
+    # the memory model's per-layer term (Eq. 12 / (tc)), from the oracle
+    layer_bytes = OM.act_bytes_per_layer(w.hidden, w.n_heads, w.n_kv_heads, w.ffn, w.seq, w.micro_batch, w.tp, w.cp)
     assert r["peak_live_stashes"] == min(pp, m) * (w.n_layers // pp)
-    assert r["peak_formula_bytes"] == r["peak_live_stashes"] * est["act_bytes_per_layer"]
-    if m >= pp:
-        assert r["peak_formula_bytes"] == w.n_layers * est["act_bytes_per_layer"]
+    assert r["peak_formula_bytes"] == r["peak_live_stashes"] * layer_bytes
+    if m >= pp:       # the first stage holds L layers (Eq. 16-17)
+        assert r["peak_formula_bytes"] == w.n_layers * layer_bytes
     assert r["peak_aux_bytes"] == r["peak_live_stashes"] * 4 * w.micro_batch * w.a_t * w.s_c
     assert arena.stats()["in_use"] == 0
     assert all(torch.isfinite(g).all() for g in grads.values())

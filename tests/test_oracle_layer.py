@@ -7,8 +7,9 @@ mathematics fixes:
   * a complex-number restatement of RoPE,
   * closed forms (equal keys -> prefix means, W = 0 -> loss = ln v),
   * float64 central finite differences of <y, dy> on tiny shards (t = 1,
-    c = 1 and c = 2 with the remote K/V as inputs),
-  * invariants (causality of the gradient, RoPE norm preservation),
+    c = 1 and c = 2 with the remote K/V as inputs; t = 2 with the sends and
+    the peers' gradient receipts in the loss),
+  * invariants (causality of dx and of dK/dV, RoPE norm preservation),
   * special cases (W_O = W_down = 0 gives y = x and dx = dy bit-exactly),
   * shard composition: t TP ranks, or c CP ranks, exchanging their true
     collective data reproduce the unsharded layer.
@@ -180,6 +181,70 @@ def test_layer_gradients_match_finite_differences(cp):
             fd = (at(1, direction) - at(-1, direction)) / (2 * eps)
             an = float(np.sum(grad * direction))
             assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, fd, an)
+
+
+@pytest.mark.parametrize("cp", [1, 2])
+def test_tensor_parallel_rank_gradients_match_finite_differences(cp):
+    # One TP rank (t = 2, rank 1) with its collective data as fixed inputs.  The
+    # backward's peer inputs are the gradients of what this rank hands to the
+    # others, so it differentiates
+    #   L = <y, dy> + <ffn_send, sp_peer_dy> + <o_send, sp_peer_dh1>
+    #       + <xn2, sp_peer_dxn2> + <xn1, sp_peer_dxn1>
+    # (the sends feed the peers' y and h1 rows; the receipts are the peers'
+    # partial gradients of this rank's normed rows).
+    sh = small_shard(tp=2, tp_rank=1, cp=cp, micro_batch=2)
+    w = make_weights(sh)
+    n_peer = (sh.t - 1) * sh.s_sp
+    x, dy = randn(sh.b, sh.s_sp, sh.h), randn(sh.b, sh.s_sp, sh.h)
+    peers = make_peers(sh)
+    for name in ("sp_peer_xn1", "sp_peer_xn2", "sp_peer_dy", "sp_peer_dh1"):
+        peers[name] = randn(sh.b, n_peer, sh.h)
+    for name in ("sp_peer_o", "sp_peer_ffn", "sp_peer_dxn2", "sp_peer_dxn1"):
+        peers[name] = randn(sh.b, sh.s_sp, sh.h)
+
+    def loss(w2, x2, p2):
+        f = Lr.layer_forward(sh, w2, x2, p2, exact=True)
+        return float(np.sum(f["y"] * dy) + np.sum(f["ffn_send"] * p2["sp_peer_dy"])
+                     + np.sum(f["o_send"] * p2["sp_peer_dh1"]) + np.sum(f["xn2"] * p2["sp_peer_dxn2"])
+                     + np.sum(f["xn1"] * p2["sp_peer_dxn1"]))
+
+    st = Lr.layer_forward(sh, w, x, peers, exact=True)
+    g = Lr.layer_backward(sh, w, st, dy, peers, exact=True)
+    grads = {"x": g["dx"], **{n: g["d_" + n] for n in w}}
+    if cp > 1:
+        grads["remote_k"], grads["remote_v"] = g["d_remote_k"], g["d_remote_v"]
+    eps = 1e-5
+    for name, grad in grads.items():
+        direction = randn(*grad.shape)
+
+        def at(sign):
+            w2, x2, p2 = dict(w), x, dict(peers)
+            if name == "x":
+                x2 = x + sign * eps * direction
+            elif name in w:
+                w2[name] = w[name] + sign * eps * direction
+            else:
+                p2[name] = peers[name] + sign * eps * direction
+            return loss(w2, x2, p2)
+        fd = (at(1) - at(-1)) / (2 * eps)
+        an = float(np.sum(grad * direction))
+        assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, fd, an)
+
+
+def test_future_keys_get_no_key_or_value_gradient():
+    # dy only in row i: K and V of every key after position i receive exactly 0
+    sh = small_shard(seq=16)
+    w = make_weights(sh)
+    x = round_bf16(randn(1, 16, sh.h))
+    dy = np.zeros((1, 16, sh.h))
+    i = 6
+    dy[0, i] = round_bf16(randn(sh.h))
+    st = Lr.layer_forward(sh, w, x)
+    g = Lr.layer_backward(sh, w, st, dy)
+    nq, nk = sh.a_t * sh.d_h, sh.k_t * sh.d_h
+    dk, dv = g["dqkv"][0, :, nq:nq + nk], g["dqkv"][0, :, nq + nk:]
+    assert np.all(dk[i + 1:] == 0.0) and np.all(dv[i + 1:] == 0.0)
+    assert np.any(dk[:i + 1] != 0.0) and np.any(dv[:i + 1] != 0.0)
 
 
 def test_gradient_is_causal():
