@@ -995,8 +995,8 @@ hipError_t bwd_impl(const AttnParams& p, int part, hipStream_t stream) {
     AttnParams q = p;
     dkdv_order(q);
     hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(blocks), dim3(512), 0, stream, q);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || p.n_split == 1) return e;
+  } else if (part == 3) {
+    if (p.n_split == 1) return hipSuccess;
     hipLaunchKernelGGL(attn_dkv_reduce_kernel<D>, dim3(p.total_keys, p.k_t, p.b), dim3(64), 0, stream, p);
   } else {
     const unsigned blocks = static_cast<unsigned>((p.n_q + 127) / 128) * p.a_t * p.b;

@@ -737,8 +737,10 @@ __device__ __forceinline__ void copy2_kc(uint8_t* lds, const Kc2Rows<WAVES>& row
 // parallel split) a lane's offset is fixed over K and across its copies up to
 // a uniform stride: copy q reads k-row kr0 + 2 * WAVES * q, and the column
 // swizzle depends on kr mod 4, which q does not change.  One offset per lane
-// is kept; each stage adds one uniform row offset.  A split operand resolves
-// every k-row through RowSrc.  The two arms issue textually different copies
+// is kept; each stage adds one uniform row offset.  A split operand whose
+// slots hold a multiple of 64 rows does the same from the mapped first row of
+// the stage; any other split operand resolves every k-row through RowSrc.  The
+// two arms issue textually different copies
 // (dma16<1> for the split one): with identical ones the compiler sinks the copy
 // below the branch and computes both addresses on every copy.
 struct Mn2Rows {
@@ -757,12 +759,26 @@ __device__ __forceinline__ Mn2Rows mn2_rows(const Operand& op, int x0, int wave,
 template <int WAVES>
 __device__ __forceinline__ void copy2_mn(uint8_t* lds, const Operand& op, const Mn2Rows& rows, int x0, int k0,
                                          int wave, int lane) {
-  if (op.src.t == 1) {       // uniform
-#pragma unroll
-    for (int q = 0; q < 32 / WAVES; ++q) {
-      const uint16_t* base = op.src.own + static_cast<int64_t>(k0 + 2 * WAVES * q) * op.src.ld;
-      dma16(base + rows.off0, lds + (wave + WAVES * q) * 1024);
+  // A stage's 64 k-rows are consecutive in memory when the operand is one
+  // plain array, and also when it is split but every sequence-parallel slot
+  // holds a multiple of 64 rows (stages start at multiples of 64, so none
+  // straddles a slot or a sequence): then the stage's first row is mapped
+  // once (uniform, scalar) and each lane adds its fixed offset.
+  if (op.src.t == 1 || op.src.s_sp % BK2 == 0) {       // uniform
+    const uint16_t* base0;
+    if (op.src.t == 1) {
+      base0 = op.src.own + static_cast<int64_t>(k0) * op.src.ld;
+    } else {
+      // pick own or peer by arithmetic on the two pointer values: a select of
+      // the members' addresses would put the kernel argument on the stack
+      const uint32_t o = op.src.row_index(k0);
+      const uint64_t own = reinterpret_cast<uint64_t>(op.src.own), peer = reinterpret_cast<uint64_t>(op.src.peer);
+      const uint64_t pick = own + ((peer - own) & (0ull - static_cast<uint64_t>(o >> 31)));
+      base0 = reinterpret_cast<const uint16_t*>(pick) + static_cast<int64_t>(o & 0x7fffffffu) * op.src.ld;
     }
+#pragma unroll
+    for (int q = 0; q < 32 / WAVES; ++q)
+      dma16(base0 + static_cast<int64_t>(2 * WAVES * q) * op.src.ld + rows.off0, lds + (wave + WAVES * q) * 1024);
     return;
   }
 #pragma unroll

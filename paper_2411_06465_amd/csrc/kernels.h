@@ -25,7 +25,7 @@ struct RowSrc {
   }
   // Row m as (index into own) or (index into peer) | 0x80000000; 32-bit arithmetic
   // (row counts are validated below 2^30 on the host).
-  __device__ inline uint32_t row_index(int64_t m64) const {
+  __device__ __forceinline__ uint32_t row_index(int64_t m64) const {
     const int32_t m = static_cast<int32_t>(m64);
     if (t == 1) return static_cast<uint32_t>(m);
     const int32_t bi = m / s_c;
@@ -35,7 +35,7 @@ struct RowSrc {
     const int32_t pi = i < lo ? i : i - s_sp;
     return static_cast<uint32_t>(bi * (t - 1) * s_sp + pi) | 0x80000000u;
   }
-  __device__ inline const uint16_t* row(int64_t m) const {
+  __device__ __forceinline__ const uint16_t* row(int64_t m) const {
     const uint32_t o = row_index(m);
     return ((o & 0x80000000u) ? peer : own) + static_cast<int64_t>(o & 0x7fffffffu) * ld;
   }
@@ -205,7 +205,8 @@ constexpr int kMaxKeyBlocks = 512;
 // Number of query-head slices the dK/dV pass uses for this shape (1 = none).
 int attn_bwd_splits(const AttnParams& p);
 hipError_t attn_fwd(const AttnParams& p, hipStream_t stream);
-// part 0: delta = rowsum(dO * O); 1: dK, dV (+ slice reduction); 2: dQ.
+// part 0: delta = rowsum(dO * O); 1: dK, dV; 3: the sum of the query-head slices
+// of dK, dV when n_split > 1 (nothing otherwise); 2: dQ.
 hipError_t attn_bwd(const AttnParams& p, int part, hipStream_t stream);
 
 // ---------------------------------------------------------------- cross-entropy
