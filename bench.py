@@ -28,6 +28,7 @@ dominant kernel's launches only in the timed steps (the roofline figure).
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline] [--no-others]
     python bench.py --workload NAME [--steps K] [--warmup W]   # one layer workload alone
+    python bench.py --norms-cold               # the RMSNorm kernels on cache-cold buffers
     python bench.py --calibrate-copy BYTES     # a plain device copy, for HBM counter calibration
     python bench.py --optimizer-only [--steps K] [--warmup W]   # the Adam step alone
 
@@ -93,8 +94,12 @@ def kernel_work(w):
     out["attn_bwd_dkdv"] = ("mfma", attn_fwd)          # dK, dV: half of the 2x-forward backward
     out["attn_bwd_dq"] = ("mfma", attn_fwd)            # dQ: the other half
     rows = w.micro_batch * w.s_sp
-    out["rmsnorm_fwd"] = ("hbm", 2 * rows * w.hidden * 2 + 2 * w.hidden)
-    out["rmsnorm_bwd"] = ("hbm", 4 * rows * w.hidden * 2 + 2 * w.hidden)
+    e, g = rows * w.hidden, 2 * w.hidden
+    parts = min(rows, 256) * w.hidden * 4                  # fp32 gain-gradient partials
+    out["rmsnorm1_fwd"] = ("hbm", 3 * e * 2 + g)           # read x; write xn1 and the stash copy of x
+    out["rmsnorm2_fwd"] = ("hbm", 2 * e * 2 + g)           # read h1; write xn2
+    out["rmsnorm2_bwd"] = ("hbm", e * (2 + 4 + 2 + 2 + 4) + g + parts)   # read h1, d(xn2) f32, dy; write dh1 bf16 + f32
+    out["rmsnorm1_bwd"] = ("hbm", e * (2 + 4 + 4 + 2) + g + parts)       # read x, d(xn1) f32, dh1 f32; write dx
     return out
 
 
@@ -263,6 +268,28 @@ def layer_entry(w, steps, warmup):
             "kernels_note": f"per-kernel table from {prof_steps} untimed steps with events around every launch; "
                             f"the timed steps carry events around {dom} only",
             "launch_sequence": sequence}
+
+
+def norms_cold(w, steps=3):
+    """The RMSNorm kernels on buffers larger than the 256 MB Infinity Cache:
+    the same layer shape at a micro-batch whose norm tensors exceed it, with
+    events around every launch; every kernel in between evicts the cache."""
+    import torch
+    _, kernels, _, _, _ = run_layer(w, 1, 1, profile=steps)
+    torch.cuda.empty_cache()
+    work = kernel_work(w)
+    out = {"workload": f"{describe(w)}; each norm tensor {w.micro_batch * w.s_sp * w.hidden * 2 / 1e6:.0f} MB",
+           "kernels": {}}
+    for k in sorted(kernels):
+        if k.startswith("rmsnorm") or k == "reduce_gain":
+            n, ms = kernels[k]
+            e = {"launches_per_step": n / steps, "us_per_launch": round(ms / n * 1e3, 1)}
+            if k in work:
+                e["algorithmic_bytes"] = work[k][1]
+                e["gbs"] = round(work[k][1] / (ms / n / 1e3) / 1e9, 1)
+                e["frac_of_hbm_peak"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
+            out["kernels"][k] = e
+    return out
 
 
 def describe(w):
@@ -520,6 +547,8 @@ def main():
     ap.add_argument("--cpu-seq", type=int, default=8192,
                     help="sequence of the oracle's CPU sample of the headline shard (8192: the whole workload)")
     ap.add_argument("--workload", default="", help="time one layer workload alone and print its object")
+    ap.add_argument("--norms-cold", action="store_true",
+                    help="time only the RMSNorm kernels on cache-cold buffers and print that object")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
     ap.add_argument("--optimizer-only", action="store_true",
                     help="time only the Adam step over the 70B optimizer shard and print its object")
@@ -543,6 +572,10 @@ def main():
               flush=True)
         return
 
+    cold = W.LLAMA2_7B.replace(name="llama2-7b-layer-b8", micro_batch=8)
+    if args.norms_cold:
+        print(json.dumps({"memory_bound_cold": norms_cold(cold)}), flush=True)
+        return
     layers = {lw.name: lw for lw in (W.LLAMA3_70B_TP8, W.LLAMA3_8B_TP2CP2, W.LLAMA2_7B)}
     if args.workload:
         if args.workload not in layers:
@@ -591,6 +624,9 @@ def main():
         others[lw.name] = {"tflops": round(lm_flops(lw) / s3 / 1e12, 2), "ms_per_step": round(s3 * 1e3, 3),
                            "pct_of_bf16_peak": round(100 * lm_flops(lw) / s3 / 1e12 / PEAK_BF16_TFLOPS, 2)}
         out["other_workloads"] = others
+        # the memory-bound kernels on cold buffers (the Llama-2-7B layer at micro-batch 8)
+        out["memory_bound_cold"] = norms_cold(cold)
+        torch.cuda.empty_cache()
         # the paper's first-stage claim, measured: 80 layer stashes of the 70B TP8 shard
         out["first_stage_1f1b"] = run_first_stage_1f1b(W.LLAMA3_70B_TP8)
         torch.cuda.empty_cache()

@@ -778,7 +778,7 @@ extern "C" int llama_layer_fwd(const l4d_model* m, const l4d_parallel* p, const 
     if ((r = launch("rope_table", s, [&] { return rope_table(rope, x.qmap, (int32_t)x.s_c, (int32_t)x.d, x.base, s); })))
       return r;
     // norm-1, stashing its input x as it goes
-    if ((r = launch("rmsnorm_fwd", s, [&] {
+    if ((r = launch("rmsnorm1_fwd", s, [&] {
            return rmsnorm_fwd(static_cast<const uint16_t*>(x_in), static_cast<const uint16_t*>(w->norm1),
                               sptr(st, L4D_STASH_XN1), x.b * x.s_sp, (int32_t)x.h, x.eps, s, sptr(st, L4D_STASH_X));
          })))
@@ -810,7 +810,7 @@ extern "C" int llama_layer_fwd(const l4d_model* m, const l4d_parallel* p, const 
                       op(RowSrc::plain(w->o, nq), x.h), Layout::KC,
                       epi_residual(x, sptr(st, L4D_STASH_H1), x_in, pi.sp_peer_o, o_send))))
       return r;
-    if ((r = launch("rmsnorm_fwd", s, [&] {
+    if ((r = launch("rmsnorm2_fwd", s, [&] {
            return rmsnorm_fwd(sptr(st, L4D_STASH_H1), static_cast<const uint16_t*>(w->norm2), sptr(st, L4D_STASH_XN2),
                               x.b * x.s_sp, (int32_t)x.h, x.eps, s);
          })))
@@ -916,7 +916,7 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
                       Layout::MN, op(xn2_full, x.h), Layout::MN, epi_acc(dw->gate_up, x.h), dwpart)))
       return r;
     // norm-2 backward + residual: dh1 in bf16 (product operand) and fp32 (residual of dx)
-    if ((r = launch("rmsnorm_bwd", s, [&] {
+    if ((r = launch("rmsnorm2_bwd", s, [&] {
            const NormBwdIo io{nullptr, dxn2, static_cast<const uint16_t*>(dy), nullptr, dh1, dh1_f32};
            return rmsnorm_bwd(sptr(st, L4D_STASH_H1), static_cast<const uint16_t*>(w->norm2), io, partial, npart,
                               rows_sp, (int32_t)x.h, x.eps, s);
@@ -970,7 +970,7 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
                       Layout::MN, epi_acc(dw->qkv, x.h), dwpart)))
       return r;
     // norm-1 backward + residual
-    if ((r = launch("rmsnorm_bwd", s, [&] {
+    if ((r = launch("rmsnorm1_bwd", s, [&] {
            const NormBwdIo io{nullptr, dxn1, nullptr, dh1_f32, static_cast<uint16_t*>(dx), nullptr};
            return rmsnorm_bwd(sptr(st, L4D_STASH_X), static_cast<const uint16_t*>(w->norm1), io, partial, npart,
                               rows_sp, (int32_t)x.h, x.eps, s);

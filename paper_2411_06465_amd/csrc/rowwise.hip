@@ -60,7 +60,7 @@ __global__ void __launch_bounds__(256) rmsnorm_fwd_kernel(const uint16_t* __rest
   for (int it = 0; it < kMaxChunks; ++it) {
     const int c = lane + 64 * it;
     if (c < nch) {
-      v[it] = xr[c];
+      v[it] = __builtin_nontemporal_load(&xr[c]);     // read once
       float f[8];
       unpack8(v[it], f);
 #pragma unroll
@@ -97,24 +97,28 @@ template <bool F32>
 struct Vec8 {
   u32x4 v;
 };
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 template <>
 struct Vec8<true> {
-  float4 a, b;
+  f32x4 a, b;
 };
 template <bool F32>
-__device__ __forceinline__ Vec8<F32> load8(const void* row, int c) {
+__device__ __forceinline__ Vec8<F32> load8(const void* row, int c) {      // read-once rows: non-temporal
   if constexpr (F32) {
-    const float4* p = reinterpret_cast<const float4*>(row) + 2 * c;
-    return Vec8<true>{p[0], p[1]};
+    const f32x4* p = reinterpret_cast<const f32x4*>(row) + 2 * c;
+    return Vec8<true>{__builtin_nontemporal_load(p), __builtin_nontemporal_load(p + 1)};
   } else {
-    return Vec8<false>{reinterpret_cast<const u32x4*>(row)[c]};
+    return Vec8<false>{__builtin_nontemporal_load(reinterpret_cast<const u32x4*>(row) + c)};
   }
 }
 template <bool F32>
 __device__ __forceinline__ void unpack(const Vec8<F32>& u, float* v) {
   if constexpr (F32) {
-    v[0] = u.a.x; v[1] = u.a.y; v[2] = u.a.z; v[3] = u.a.w;
-    v[4] = u.b.x; v[5] = u.b.y; v[6] = u.b.z; v[7] = u.b.w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[i] = u.a[i];
+      v[4 + i] = u.b[i];
+    }
   } else {
     unpack8(u.v, v);
   }
@@ -157,7 +161,7 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
     for (int it = 0; it < CPT; ++it) {
       const int c = tid + 256 * it;
       if (c < nch) {
-        a[it] = xr[c];
+        a[it] = __builtin_nontemporal_load(&xr[c]);
         b[it] = load8<DY32>(dr, c);
         if constexpr (RES != 0) r[it] = load8<R32>(rr, c);
       }
