@@ -34,7 +34,8 @@
 // or a gate/up pair of the fused FFN weight.  The epilogue stages rows through
 // LDS and hands 8-column vectors to the fused operation, with that operation's
 // global inputs loaded for a whole pass first.  The fp32 accumulate (dW) needs
-// no staging: the accumulators start from the C tile and are stored back.
+// no staging: the C tile meets the accumulators in registers (added at the end
+// in the BK = 64 kernel, loaded before the first product in the BK = 32 one).
 #include "kernels.h"
 
 namespace l4d {
@@ -486,9 +487,10 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, f32x16 (&acc)[4]
   }
 }
 
-// AccF32 (C += A B^T in fp32) works on the accumulators directly: the tile of C
-// is loaded into them before the first product (its latency overlaps the first
-// stage's copies) and stored from them at the end.  In the accumulator layout
+// AccF32 (C += A B^T in fp32) works on the accumulators directly.  In the BK =
+// 32 kernel the tile of C is loaded into them before the first product (its
+// latency overlaps the first stage's copies) and stored from them at the end;
+// the BK = 64 kernel adds it at the end (acc_add_store_f32).  In the accumulator layout
 // the 32 lanes of a half-wave cover 32 consecutive columns (128 bytes) of one
 // row, so both are whole-line accesses without staging.  Whole tiles load and
 // store non-temporally: each C element is touched once per launch, and
@@ -546,6 +548,65 @@ __device__ __forceinline__ void acc_store_f32(const f32x16 (&acc)[4][NS], const 
       for (int ns = 0; ns < NS; ++ns) {
         const int n = tn * BN + ncol[ns] + (lane & 31);
         if (full || (row0 + r + rl < p.M && n < p.N)) __builtin_nontemporal_store(acc[ms][ns][i], &row[off[ns]]);
+      }
+    }
+}
+
+// acc + C -> C for a tile whose products started from zero, one accumulator
+// row block (32 rows) at a time.  Whole tiles are software-pipelined: the
+// loads of block ms + 1 are issued before the stores of block ms, so that
+// waiting for a block's C values (the wait counter also counts stores) does
+// not wait for the stores issued after them.  They go through a buffer
+// descriptor of the wave's 128 rows: the row offset is a scalar, the lane
+// offset one register per column block, which leaves the registers for the
+// two blocks of C in flight.  Edge tiles go element by element.
+constexpr int kBufNT = 2;   // cache-policy bit of a non-temporal buffer access
+template <int NS>
+__device__ __forceinline__ void acc_add_store_f32(const f32x16 (&acc)[4][NS], const GemmParams& p, float* cbase,
+                                                  int64_t ldc, int64_t row0, int tn, const int* ncol, int lane) {
+  const int rl = 4 * (lane >> 5);
+  if (row0 + 128 <= p.M && (tn + 1) * BN <= p.N) {   // uniform
+    const __amdgpu_buffer_rsrc_t win =
+        __builtin_amdgcn_make_buffer_rsrc(cbase + row0 * ldc, 0, static_cast<int>(0x7fffffff), 0x00020000);
+    int32_t voff[NS];   // lane's byte offset in its row
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns) voff[ns] = (static_cast<int32_t>(rl * ldc) + tn * BN + ncol[ns] + (lane & 31)) * 4;
+    const int32_t ldc4 = static_cast<int32_t>(ldc * 4);
+    float c[2][16][NS];   // the buffer builtins move 32-bit words: bit casts, not conversions
+    auto load = [&](int ms, float (&cb)[16][NS]) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+#pragma unroll
+        for (int ns = 0; ns < NS; ++ns)
+          cb[i][ns] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                       win, voff[ns], (ms * 32 + 8 * (i >> 2) + (i & 3)) * ldc4, kBufNT));
+    };
+    load(0, c[0]);
+#pragma unroll
+    for (int ms = 0; ms < 4; ++ms) {
+      if (ms + 1 < 4) load(ms + 1, c[(ms + 1) & 1]);
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+#pragma unroll
+        for (int ns = 0; ns < NS; ++ns)
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, acc[ms][ns][i] + c[ms & 1][i][ns]), win,
+                                                voff[ns], (ms * 32 + 8 * (i >> 2) + (i & 3)) * ldc4, kBufNT);
+    }
+    return;
+  }
+  int32_t off[NS];
+#pragma unroll
+  for (int ns = 0; ns < NS; ++ns) off[ns] = static_cast<int32_t>(rl * ldc) + tn * BN + ncol[ns] + (lane & 31);
+#pragma unroll
+  for (int ms = 0; ms < 4; ++ms)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = ms * 32 + 8 * (i >> 2) + (i & 3);
+      float* row = cbase + (row0 + r) * ldc;
+#pragma unroll
+      for (int ns = 0; ns < NS; ++ns) {
+        const int n = tn * BN + ncol[ns] + (lane & 31);
+        if (row0 + r + rl < p.M && n < p.N) row[off[ns]] += acc[ms][ns][i];
       }
     }
 }
@@ -850,9 +911,8 @@ __device__ __forceinline__ void interleave2() {
 
 // The BK = 64 main loop of one tile over its stages [kb, kb + n), n even:
 // products added into acc.  The four stage buffers a0 b0 a1 b1 (32 KB each)
-// hold two stages.  SETTLE: acc holds a C tile still being loaded (the fp32
-// accumulate), settled after the first stage's copies.
-template <Layout LA, Layout LB, int WAVES, bool SETTLE>
+// hold two stages.
+template <Layout LA, Layout LB, int WAVES>
 __device__ __forceinline__ void mainloop64(const GemmParams& p, f32x16 (&acc)[4][WAVES == 8 ? 2 : 4], int tm, int tn,
                                            int kb, int n, uint8_t* a0, uint8_t* b0, uint8_t* a1, uint8_t* b1,
                                            int wave, int lane, int wm, const int* ncol) {
@@ -913,7 +973,6 @@ __device__ __forceinline__ void mainloop64(const GemmParams& p, f32x16 (&acc)[4]
 
   issue_a(0, a0);
   issue_b(0, b0);
-  if constexpr (SETTLE) settle_acc<NS>(acc);   // the C tile (and stage 0) have landed
   issue_a(1, a1);
   issue_b(1, b1);
   if constexpr (PER == 8) wait_vm<16>();
@@ -972,17 +1031,20 @@ __global__ void __launch_bounds__(WAVES * 64, 1) gemm_bk64(GemmParams p) {
   }
 
   f32x16 acc[4][NS];
-  if (KIND == EpiKind::AccF32 && part == 0) {
-    acc_load_f32<NS>(acc, p, cbase, ldc, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
-  } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
-  }
+    for (int j = 0; j < NS; ++j) acc[i][j] = f32x16{};
   // K is a multiple of 2 * BK2 * parts (the host picks this kernel only then).
-  mainloop64<LA, LB, WAVES, KIND == EpiKind::AccF32>(p, acc, tm, tn, part * n_st, n_st, a0, b0, a1, b1, wave,
-                                                             lane, wm, ncol);
+  mainloop64<LA, LB, WAVES>(p, acc, tm, tn, part * n_st, n_st, a0, b0, a1, b1, wave, lane, wm, ncol);
+  // The fp32 accumulate: the products start from zero and part 0 adds the C
+  // tile in the epilogue, whose loads overlap its stores (loading C into the
+  // accumulators before the first product measured 2-3% slower on the largest
+  // weight-gradient GEMMs of the Llama-3-70B TP8 shard).
+  if (KIND == EpiKind::AccF32 && part == 0) {
+    acc_add_store_f32<NS>(acc, p, cbase, ldc, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
+    return;
+  }
   if (KIND == EpiKind::AccF32 || (KIND == EpiKind::StoreBF16 && parts > 1)) {
     acc_store_f32<NS>(acc, p, cbase, ldc, static_cast<int64_t>(m0) + wm * 128, tn, ncol, lane);
   } else {
@@ -1003,6 +1065,8 @@ hipError_t launch(const GemmParams& p, hipStream_t stream) {
   if (parts > 1 && ((KIND != EpiKind::AccF32 && KIND != EpiKind::StoreBF16) || p.K % (2 * BK2 * parts) != 0 ||
                     !p.partial))
     return hipErrorInvalidValue;
+  // the fp32 accumulate's whole-tile epilogue addresses 128 rows of C with 32-bit byte offsets
+  if (KIND == EpiKind::AccF32 && p.epi.ldc > (int64_t{1} << 21)) return hipErrorInvalidValue;
   const dim3 grid(tiles_m * tiles_n * parts);
   if (p.K % (2 * BK2) == 0)
     hipLaunchKernelGGL((gemm_bk64<LA, LB, KIND, PAIR, 8>), grid, dim3(512), 0, stream, p);
