@@ -9,7 +9,8 @@ import ctypes as C
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libl4d.so")
+# L4D_LIB names another build of the same sources (the host-sanitizer build of the tests)
+LIB_PATH = os.environ.get("L4D_LIB") or os.path.join(_HERE, "libl4d.so")
 
 L4D_OK, L4D_EINVAL, L4D_ENOMEM, L4D_EDEVICE = 0, 1, 2, 3
 STASH_NAMES = ["x", "xn1", "q", "k", "v", "ctx", "h1", "xn2", "gate", "up", "act", "prod", "lse"]

@@ -120,6 +120,10 @@ def test_stash_bytes_equal_the_activation_formula(w):
     for (p0, n0), (p1, _) in zip(spans, spans[1:]):
         assert p0 + n0 <= p1
     assert spans[0][0] >= FAKE_BASE
+    for bad in (-1, len(L.STASH_NAMES)):     # one past the last tensor is refused, not read
+        with pytest.raises(L.L4DError) as e:
+            st.tensor(bad)
+        assert e.value.code == L.L4D_EINVAL
     st.release()
     assert a.stats()["in_use"] == 0
     a.destroy()
