@@ -45,22 +45,40 @@ constexpr int kMaxChunks = 16;   // h <= 64 lanes * 16 chunks * 8 = 8192
 
 // ------------------------------------------------------------------ RMSNorm
 
+// One wave per row.  All of the row's loads are issued before the first use,
+// so that a wave keeps its whole row (8 KB at h = 4096) in flight: a use right
+// after each load waits for it and leaves one kilobyte in flight per wave.
+// CPT > 0: h = 512 CPT (every lane holds CPT chunks, no bounds); CPT = 0: any
+// h that is a multiple of 8.
+template <int CPT>
 __global__ void __launch_bounds__(256) rmsnorm_fwd_kernel(const uint16_t* __restrict__ x,
                                                           const uint16_t* __restrict__ gain,
                                                           uint16_t* __restrict__ y, uint16_t* __restrict__ x_copy,
                                                           int64_t rows, int32_t h, float eps) {
+  constexpr int NC = CPT > 0 ? CPT : kMaxChunks;
   const int lane = threadIdx.x & 63;
   const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
-  const int nch = h / 8;
+  const int nch = CPT > 0 ? 64 * CPT : h / 8;
   const u32x4* xr = reinterpret_cast<const u32x4*>(x + row * h);
-  u32x4 v[kMaxChunks];
+  const u32x4* gr = reinterpret_cast<const u32x4*>(gain);
+  u32x4 v[NC], gv[NC];
+#pragma unroll
+  for (int it = 0; it < NC; ++it) {
+    const int c = lane + 64 * it;
+    if (CPT > 0 || c < nch) v[it] = __builtin_nontemporal_load(&xr[c]);     // read once
+  }
+  // the gain too, before any store: a load issued after a store waits for it
+#pragma unroll
+  for (int it = 0; it < NC; ++it) {
+    const int c = lane + 64 * it;
+    if (CPT > 0 || c < nch) gv[it] = gr[c];
+  }
   float ss = 0.f;
 #pragma unroll
-  for (int it = 0; it < kMaxChunks; ++it) {
+  for (int it = 0; it < NC; ++it) {
     const int c = lane + 64 * it;
-    if (c < nch) {
-      v[it] = __builtin_nontemporal_load(&xr[c]);     // read once
+    if (CPT > 0 || c < nch) {
       float f[8];
       unpack8(v[it], f);
 #pragma unroll
@@ -70,21 +88,20 @@ __global__ void __launch_bounds__(256) rmsnorm_fwd_kernel(const uint16_t* __rest
   if (x_copy) {     // the input, kept for the backward
     u32x4* cr = reinterpret_cast<u32x4*>(x_copy + row * h);
 #pragma unroll
-    for (int it = 0; it < kMaxChunks; ++it) {
+    for (int it = 0; it < NC; ++it) {
       const int c = lane + 64 * it;
-      if (c < nch) cr[c] = v[it];
+      if (CPT > 0 || c < nch) cr[c] = v[it];
     }
   }
   const float rstd = rsqrtf(wave_sum(ss) / h + eps);
-  const u32x4* gr = reinterpret_cast<const u32x4*>(gain);
   u32x4* yr = reinterpret_cast<u32x4*>(y + row * h);
 #pragma unroll
-  for (int it = 0; it < kMaxChunks; ++it) {
+  for (int it = 0; it < NC; ++it) {
     const int c = lane + 64 * it;
-    if (c < nch) {
+    if (CPT > 0 || c < nch) {
       float f[8], g[8];
       unpack8(v[it], f);
-      unpack8(gr[c], g);
+      unpack8(gv[it], g);
 #pragma unroll
       for (int j = 0; j < 8; ++j) f[j] = f[j] * rstd * g[j];
       yr[c] = pack8(f);
@@ -587,8 +604,12 @@ __global__ void __launch_bounds__(256) embed_bwd_kernel(const int64_t* __restric
 hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* gain, uint16_t* y, int64_t rows, int32_t h,
                        float eps, hipStream_t stream, uint16_t* x_copy) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(rmsnorm_fwd_kernel, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream,
-                     x, gain, y, x_copy, rows, h, eps);
+  const dim3 grid(static_cast<unsigned>((rows + 3) / 4));
+  switch (h % 512 == 0 ? h / 512 : 0) {
+    case 8: hipLaunchKernelGGL(rmsnorm_fwd_kernel<8>, grid, dim3(256), 0, stream, x, gain, y, x_copy, rows, h, eps); break;
+    case 16: hipLaunchKernelGGL(rmsnorm_fwd_kernel<16>, grid, dim3(256), 0, stream, x, gain, y, x_copy, rows, h, eps); break;
+    default: hipLaunchKernelGGL(rmsnorm_fwd_kernel<0>, grid, dim3(256), 0, stream, x, gain, y, x_copy, rows, h, eps);
+  }
   return hipGetLastError();
 }
 
