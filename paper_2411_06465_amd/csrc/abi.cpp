@@ -956,10 +956,10 @@ extern "C" int llama_layer_bwd(const l4d_model* m, const l4d_parallel* p, const 
       ap.dkv_partial = reinterpret_cast<float*>(wsb + plan.dkv);
       ap.partial_half = (int64_t)ap.n_split * x.b * ap.total_keys * x.k_t * x.d;
     }
-    if ((r = launch("attn_bwd_delta", s, [&] { return attn_bwd(ap, 0, s); }))) return r;
+    // dQ first: it also writes delta = rowsum(dO * O), which dK/dV reads
+    if ((r = launch("attn_bwd_dq", s, [&] { return attn_bwd(ap, 2, s); }))) return r;
     if ((r = launch("attn_bwd_dkdv", s, [&] { return attn_bwd(ap, 1, s); }))) return r;
     if (ap.n_split > 1 && (r = launch("attn_dkv_reduce", s, [&] { return attn_bwd(ap, 3, s); }))) return r;
-    if ((r = launch("attn_bwd_dq", s, [&] { return attn_bwd(ap, 2, s); }))) return r;
     // QKV projection
     if ((r = run_gemm("gemm_qkv_dx", s, tok, x.h, qc, op(RowSrc::plain(dqkv, qc), tok), Layout::KC,
                       op(RowSrc::plain(w->qkv, x.h), x.h), Layout::MN,

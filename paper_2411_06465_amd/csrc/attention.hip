@@ -509,32 +509,6 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
 }
 
-// ------------------------------------------------------------------ backward: delta
-// delta[b][h][q] = sum_d dO[q][h*D + d] * O[q][h*D + d]; one wave per (b, q) row.
-template <int D>
-__global__ void __launch_bounds__(256) attn_delta_kernel(AttnParams p) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (row >= static_cast<int64_t>(p.b) * p.n_q) return;
-  const int64_t bi = row / p.n_q, q = row % p.n_q;
-  const uint16_t* o = p.o + bi * p.q_bstride + q * p.q_ld;
-  const uint16_t* d = p.dout + bi * p.q_bstride + q * p.q_ld;
-  constexpr int CPH = D / 8;
-  const int nch = p.a_t * CPH;
-  for (int c0 = 0; c0 < nch; c0 += 64) {
-    const int c = c0 + lane;
-    float s = 0.f;
-    if (c < nch) {
-      const u32x4 a = *reinterpret_cast<const u32x4*>(o + c * 8);
-      const u32x4 b = *reinterpret_cast<const u32x4*>(d + c * 8);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) s += lo16(a[j]) * lo16(b[j]) + hi16(a[j]) * hi16(b[j]);
-    }
-#pragma unroll
-    for (int off = CPH / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-    if (c < nch && (c % CPH) == 0) p.delta[(bi * p.a_t + c / CPH) * p.n_q + q] = s;
-  }
-}
 
 // ------------------------------------------------------------------ backward: dK, dV
 // Flat grid over (key block of 128 over all segments, kv head, split, b), key
@@ -838,6 +812,9 @@ __global__ void __launch_bounds__(64) attn_dkv_reduce_kernel(AttnParams p) {
 // keep Q, dO, dQ and the two score tiles within 256 registers, so two
 // workgroups share a CU.  Per tile: S^T = K Q^T and dP^T = V dO^T, then
 // dS^T = P^T (dP^T - delta) feeds dQ^T += K^T dS^T from registers.
+// delta = rowsum(dO * O) of the block's queries is formed here, from the dO
+// fragments it holds anyway and the matching fragments of O, and written out
+// for the dK/dV pass, which runs after this one.
 template <int D>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) attn_bwd_dq_kernel(AttnParams p) {
   constexpr int KQ = 32;                     // keys per tile
@@ -860,18 +837,29 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))
   const LaneAddr la = lane_addr<D>(lane);
 
   bf16x8 qf[D / 16], dof[D / 16];
+  float my_delta = 0.f;
   {
     const int64_t off = bi * p.q_bstride + static_cast<int64_t>(q_ok ? my_q : 0) * p.q_ld + hq * D;
+    u32x4 of[D / 16];
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       const int dcol = (2 * kk + (lane >> 5)) * 8;
       qf[kk] = *reinterpret_cast<const bf16x8*>(p.q + off + dcol);
       dof[kk] = *reinterpret_cast<const bf16x8*>(p.dout + off + dcol);
+      of[kk] = *reinterpret_cast<const u32x4*>(p.o + off + dcol);
     }
+    // the lane's half of the row (8-column chunks of one parity), then its partner's half
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      const u32x4 g = __builtin_bit_cast(u32x4, dof[kk]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) my_delta += lo16(g[j]) * lo16(of[kk][j]) + hi16(g[j]) * hi16(of[kk][j]);
+    }
+    my_delta += __shfl_xor(my_delta, 32, 64);
   }
   const int64_t sidx = (static_cast<int64_t>(bi) * p.a_t + hq) * p.n_q + (q_ok ? my_q : 0);
   const float my_lse = p.lse[sidx] * kLog2e;
-  const float my_delta = p.delta[sidx];
+  if (q_ok && lane < 32) p.delta[sidx] = my_delta;
 #pragma unroll
   for (int kk = 0; kk < D / 16; ++kk) {
     settle(qf[kk]);
@@ -987,10 +975,7 @@ void dkdv_order(AttnParams& p) {
 
 template <int D>
 hipError_t bwd_impl(const AttnParams& p, int part, hipStream_t stream) {
-  if (part == 0) {
-    const int64_t rows = static_cast<int64_t>(p.b) * p.n_q;
-    hipLaunchKernelGGL(attn_delta_kernel<D>, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, p);
-  } else if (part == 1) {
+  if (part == 1) {
     const unsigned blocks = static_cast<unsigned>(count_blocks(p, 128)) * p.k_t * p.n_split * p.b;
     AttnParams q = p;
     dkdv_order(q);

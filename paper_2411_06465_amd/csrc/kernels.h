@@ -205,8 +205,8 @@ constexpr int kMaxKeyBlocks = 512;
 // Number of query-head slices the dK/dV pass uses for this shape (1 = none).
 int attn_bwd_splits(const AttnParams& p);
 hipError_t attn_fwd(const AttnParams& p, hipStream_t stream);
-// part 0: delta = rowsum(dO * O); 1: dK, dV; 3: the sum of the query-head slices
-// of dK, dV when n_split > 1 (nothing otherwise); 2: dQ.
+// part 2: dQ, and delta = rowsum(dO * O) for part 1; 1: dK, dV (after part 2);
+// 3: the sum of the query-head slices of dK, dV when n_split > 1 (nothing otherwise).
 hipError_t attn_bwd(const AttnParams& p, int part, hipStream_t stream);
 
 // ---------------------------------------------------------------- cross-entropy
