@@ -164,11 +164,11 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[it][j] = 0.f;
   const u32x4* gr = reinterpret_cast<const u32x4*>(gain);
-  u32x4 gv[CPT], xv[CPT], xn[CPT];
-  Vec8<DY32> dv[CPT], dn[CPT];
-  Vec8<R32> rv[CPT], rn[CPT];
+  u32x4 gv[CPT];
   const int64_t dsz = DY32 ? 4 : 2, rsz = R32 ? 4 : 2;
-  // row `row`'s x, d(out) and residual gradient into (a, b, r)
+  // row `row`'s x, d(out) and residual gradient into (a, b, r); every lane
+  // loads (a lane past the row end reloads the row's last chunk, unused), so
+  // the number of loads in flight is fixed and the waits for a row count exactly
   auto load_row = [&](int64_t row, u32x4 (&a)[CPT], Vec8<DY32> (&b)[CPT], Vec8<R32> (&r)[CPT])
                       __attribute__((always_inline)) {
     const u32x4* xr = reinterpret_cast<const u32x4*>(x + row * h);
@@ -176,30 +176,21 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
     const void* rr = RES ? static_cast<const uint8_t*>(dres) + row * h * rsz : nullptr;
 #pragma unroll
     for (int it = 0; it < CPT; ++it) {
-      const int c = tid + 256 * it;
-      if (c < nch) {
-        a[it] = __builtin_nontemporal_load(&xr[c]);
-        b[it] = load8<DY32>(dr, c);
-        if constexpr (RES != 0) r[it] = load8<R32>(rr, c);
-      }
+      const int c = min(tid + 256 * it, nch - 1);
+      a[it] = __builtin_nontemporal_load(&xr[c]);
+      b[it] = load8<DY32>(dr, c);
+      if constexpr (RES != 0) r[it] = load8<R32>(rr, c);
     }
   };
 #pragma unroll
-  for (int it = 0; it < CPT; ++it) {
-    const int c = tid + 256 * it;
-    if (c < nch) gv[it] = gr[c];
-  }
+  for (int it = 0; it < CPT; ++it) gv[it] = gr[min(tid + 256 * it, nch - 1)];
   int parity = 0;
-  if (static_cast<int64_t>(blockIdx.x) < rows) load_row(blockIdx.x, xn, dn, rn);
-  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x, parity ^= 1) {
-#pragma unroll
-    for (int it = 0; it < CPT; ++it) {
-      xv[it] = xn[it];
-      dv[it] = dn[it];
-      if constexpr (RES != 0) rv[it] = rn[it];
-    }
-    // the next row's loads fly under this row's reductions and stores
-    if (row + gridDim.x < rows) load_row(row + gridDim.x, xn, dn, rn);
+  // one row: the two row sums, then dx and the gain partials.  A lane past the
+  // row end holds a copy of the last chunk (loads clamped), so it stores the
+  // same values to the same place as the chunk's own lane, and no store is
+  // conditional; it leaves the row sums and the gain partials alone.
+  auto process = [&](int64_t row, const u32x4 (&xv)[CPT], const Vec8<DY32> (&dv)[CPT], const Vec8<R32> (&rv)[CPT])
+                     __attribute__((always_inline)) {
     float ss = 0.f, dot = 0.f;
 #pragma unroll
     for (int it = 0; it < CPT; ++it) {
@@ -225,36 +216,78 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(
     __syncthreads();
     ss = (sums[parity][0][0] + sums[parity][1][0]) + (sums[parity][2][0] + sums[parity][3][0]);
     dot = (sums[parity][0][1] + sums[parity][1][1]) + (sums[parity][2][1] + sums[parity][3][1]);
+    parity ^= 1;
     const float rstd = rsqrtf(ss / h + eps);
     const float c_mean = dot * rstd / h;        // mean over the row of (gain*dy) * xhat
     u32x4* out = reinterpret_cast<u32x4*>(dx + row * h);
     float4* out32 = OUT32 ? reinterpret_cast<float4*>(dx32 + row * h) : nullptr;
 #pragma unroll
     for (int it = 0; it < CPT; ++it) {
-      const int c = tid + 256 * it;
-      if (c < nch) {
-        float f[8], d[8], g[8], r[8];
-        unpack8(xv[it], f);
-        unpack<DY32>(dv[it], d);
-        unpack8(gv[it], g);
-        if constexpr (RES != 0) {
-          unpack<R32>(rv[it], r);
-        } else {
+      const int c = min(tid + 256 * it, nch - 1);
+      const float own = tid + 256 * it < nch ? 1.f : 0.f;
+      float f[8], d[8], g[8], r[8];
+      unpack8(xv[it], f);
+      unpack<DY32>(dv[it], d);
+      unpack8(gv[it], g);
+      if constexpr (RES != 0) {
+        unpack<R32>(rv[it], r);
+      } else {
 #pragma unroll
-          for (int j = 0; j < 8; ++j) r[j] = 0.f;
-        }
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float xh = f[j] * rstd;
-          acc[it][j] += d[j] * xh;
-          r[j] += rstd * (g[j] * d[j] - xh * c_mean);
-        }
-        out[c] = pack8(r);
-        if constexpr (OUT32) {
-          out32[2 * c] = make_float4(r[0], r[1], r[2], r[3]);
-          out32[2 * c + 1] = make_float4(r[4], r[5], r[6], r[7]);
-        }
+        for (int j = 0; j < 8; ++j) r[j] = 0.f;
       }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float xh = f[j] * rstd;
+        acc[it][j] += own * (d[j] * xh);
+        r[j] += rstd * (g[j] * d[j] - xh * c_mean);
+      }
+      out[c] = pack8(r);
+      if constexpr (OUT32) {
+        out32[2 * c] = make_float4(r[0], r[1], r[2], r[3]);
+        out32[2 * c + 1] = make_float4(r[4], r[5], r[6], r[7]);
+      }
+    }
+  };
+  const int64_t G = gridDim.x, last = rows - 1;
+  if constexpr (CPT <= 2 && DY32 && RES == 2) {
+    // The read-heaviest form (10 of its 12 bytes per element are reads) keeps
+    // two rows in flight, in three register sets: rows row + G and row + 2G
+    // load while row is processed (a load past the last row reloads the last
+    // row, unused).  On 268 MB cache-cold tensors: 302 -> 287 us; the lighter
+    // forms measured no better.
+    u32x4 xa[CPT], xb[CPT], xc[CPT];
+    Vec8<DY32> da[CPT], db[CPT], dc[CPT];
+    Vec8<R32> ra[CPT], rb[CPT], rc[CPT];
+    int64_t row = blockIdx.x;
+    if (row < rows) {
+      load_row(row, xa, da, ra);
+      load_row(min(row + G, last), xb, db, rb);
+    }
+    for (; row < rows; row += 3 * G) {
+      load_row(min(row + 2 * G, last), xc, dc, rc);
+      process(row, xa, da, ra);
+      if (row + G >= rows) break;
+      load_row(min(row + 3 * G, last), xa, da, ra);
+      process(row + G, xb, db, rb);
+      if (row + 2 * G >= rows) break;
+      load_row(min(row + 4 * G, last), xb, db, rb);
+      process(row + 2 * G, xc, dc, rc);
+    }
+  } else {
+    u32x4 xv[CPT], xn[CPT];
+    Vec8<DY32> dv[CPT], dn[CPT];
+    Vec8<R32> rv[CPT], rn[CPT];
+    if (static_cast<int64_t>(blockIdx.x) < rows) load_row(blockIdx.x, xn, dn, rn);
+    for (int64_t row = blockIdx.x; row < rows; row += G) {
+#pragma unroll
+      for (int it = 0; it < CPT; ++it) {
+        xv[it] = xn[it];
+        dv[it] = dn[it];
+        if constexpr (RES != 0) rv[it] = rn[it];
+      }
+      // the next row's loads fly under this row's reductions and stores
+      if (row + G < rows) load_row(row + G, xn, dn, rn);
+      process(row, xv, dv, rv);
     }
   }
   float* pr = partial + static_cast<int64_t>(blockIdx.x) * h;
