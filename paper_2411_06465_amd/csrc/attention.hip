@@ -235,21 +235,6 @@ __device__ __forceinline__ bool find_tile(const AttnParams& p, int tile, int tsz
   }
   return false;
 }
-__device__ __forceinline__ int total_tiles(const AttnParams& p, int tsz) {
-  int acc = 0;
-  for (int s = 0; s < p.n_seg; ++s) acc += (p.seg[s].n + tsz - 1) / tsz;
-  return acc;
-}
-// Next key tile at or after `from` whose first key a query at pos_max can see.
-__device__ __forceinline__ int next_key_tile(const AttnParams& p, int from, int ntiles, int pos_max, int& seg,
-                                             int& t0) {
-  for (int t = from; t < ntiles; ++t) {
-    if (!find_tile(p, t, KT, seg, t0)) break;
-    if (p.seg[seg].pos0 + t0 <= pos_max) return t;
-  }
-  return ntiles;
-}
-
 
 // ------------------------------------------------------------------ forward
 // One workgroup per (128-query tile, query head, batch element); 4 waves x 32
